@@ -1,0 +1,75 @@
+"""Pins of the paged latent layout (a stated reading; the paper fixes none)."""
+
+import numpy as np
+import pytest
+
+from oracle import layout
+
+
+@pytest.mark.parametrize("RK, rv", [(1, 1), (7, 3), (8, 8), (43, 17), (128, 128), (1228, 1536)])
+def test_offsets_are_a_bijection_onto_the_page(RK, rv):
+    RKp = layout.key_row_stride(RK)
+    assert RKp % 8 == 0 and RK <= RKp < RK + 8
+    n = layout.page_elems(RK, rv)
+    used = np.zeros(n, dtype=np.int64)
+    s = np.arange(64)[:, None]
+    used_k = layout.key_offset(s, np.arange(RK)[None, :], RK).ravel()
+    used_v = layout.value_offset(s, np.arange(rv)[None, :], RK).ravel()
+    np.add.at(used, used_k, 1)
+    np.add.at(used, used_v, 1)
+    # every latent element has its own slot; the only unused slots are the
+    # key-row padding columns RK..RKp-1
+    assert used.max() == 1
+    pad = np.flatnonzero(used == 0)
+    expect_pad = (np.arange(64)[:, None] * RKp + np.arange(RK, RKp)[None, :]).ravel()
+    assert np.array_equal(np.sort(pad), np.sort(expect_pad))
+
+
+def test_hand_offsets():
+    # R_K = 10 -> rows of 16; r_v = 3
+    assert layout.key_row_stride(10) == 16
+    assert layout.page_elems(10, 3) == 64 * 16 + 64 * 3
+    assert layout.key_offset(0, 0, 10) == 0
+    assert layout.key_offset(2, 9, 10) == 2 * 16 + 9
+    assert layout.value_offset(0, 0, 10) == 1024
+    assert layout.value_offset(5, 2, 10) == 1024 + 2 * 64 + 5
+
+
+def test_pack_unpack_through_permuted_pages():
+    g = np.random.default_rng(0)
+    RK, rv, lens = 13, 9, [1, 64, 65, 200]
+    pages = [-(-t // 64) for t in lens]
+    phys = g.permutation(sum(pages))
+    table = np.zeros((len(lens), max(pages)), dtype=np.int32)
+    pos = 0
+    for b, n in enumerate(pages):
+        table[b, :n] = phys[pos:pos + n]
+        pos += n
+    pool = layout.new_pool(sum(pages), RK, rv)
+    data = []
+    for b, T in enumerate(lens):
+        Zk = g.standard_normal((T, RK))
+        Zv = g.standard_normal((T, rv))
+        # write in two uneven pieces to cross page boundaries mid-call
+        cut = T // 3
+        layout.pack(pool, table, b, 0, Zk[:cut], Zv[:cut])
+        layout.pack(pool, table, b, cut, Zk[cut:], Zv[cut:])
+        data.append((Zk, Zv))
+    for b, T in enumerate(lens):
+        Zk, Zv = layout.unpack(pool, table, b, T, RK, rv)
+        assert np.array_equal(Zk, data[b][0]) and np.array_equal(Zv, data[b][1])
+        # element-by-element against the offset functions
+        for t in range(0, T, 17):
+            page, s = table[b, t // 64], t % 64
+            for k in range(RK):
+                assert pool[page, layout.key_offset(s, k, RK)] == data[b][0][t, k]
+            for j in range(rv):
+                assert pool[page, layout.value_offset(s, j, RK)] == data[b][1][t, j]
+    # untouched slots (padding columns, slots past each length) stay zero
+    written = np.zeros_like(pool, dtype=bool)
+    for b, T in enumerate(lens):
+        for t in range(T):
+            page, s = table[b, t // 64], t % 64
+            written[page, layout.key_offset(s, np.arange(RK), RK)] = True
+            written[page, layout.value_offset(s, np.arange(rv), RK)] = True
+    assert np.all(pool[~written] == 0)
