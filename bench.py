@@ -1,0 +1,246 @@
+#!/usr/bin/env python3
+"""Benchmark of the compressed-KV decode hot path on one MI355X.
+
+One step = the whole hot path over one batch of synthetic input:
+latent_append of the workload's new tokens (z = x [L_K | L_v] into the paged
+cache) followed by one decode over every sequence's full context (fold,
+split-K attention over the latents, fixed-order merge, up-projection).
+Default workload: long-context MHA, 32 heads x 128, one sequence of 131072
+tokens whose last 512 are appended in the step, 6 key groups with ranks
+summing to 1536, value rank 2048, bf16 latents.
+
+Prints one JSON line.  `value` is decode tokens/s (sequences decoded per
+second of step time) with every input resident in HBM before timing starts.
+`roofline` covers the split-K attention kernel, timed with HIP events
+recorded around each of its launches on the decode stream.  `cpu_baseline`
+times the fp64 CPU oracle on a bounded sample of the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="mha_long_t128k")
+    ap.add_argument("--split-tokens", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target CPU time of the oracle sample")
+    return ap.parse_args()
+
+
+def device_inputs(wl, plan, torch):
+    """Synthetic device tensors of the workload's shapes (seeded)."""
+    from workloads.inputs import random_pool_fill
+    dev = "cuda"
+    g = torch.Generator(device=dev)
+    g.manual_seed(1000 + wl.seed)
+    tdt = plan.torch_dtype
+    pool = random_pool_fill(wl.total_pages, plan.page_elems, wl.dtype, seed=wl.seed, device=dev)
+    pages = wl.pages_per_seq
+    table = torch.zeros((wl.batch, wl.max_pages), dtype=torch.int32)
+    pos = 0
+    for b, n in enumerate(pages):
+        table[b, :n] = torch.arange(pos, pos + n, dtype=torch.int32)
+        pos += n
+    d = dict(
+        pool=pool,
+        page_table=table.to(dev),
+        seq_lens=torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev),
+        q=torch.randn((wl.batch, wl.num_q_heads, wl.head_dim), generator=g, device=dev),
+        R_keys=(torch.randn(plan.key_factor_elems, generator=g, device=dev) * 0.05).to(tdt),
+        R_value=(torch.randn((wl.value_rank, wl.kv_dim), generator=g, device=dev) * 0.02).to(tdt),
+    )
+    if wl.append_tokens:
+        d["x"] = torch.randn((wl.append_tokens, wl.hidden), generator=g, device=dev).to(tdt)
+        d["L_keys"] = (torch.randn((wl.hidden, wl.key_rank_total), generator=g, device=dev)
+                       / math.sqrt(wl.hidden)).to(tdt)
+        d["L_value"] = (torch.randn((wl.hidden, wl.value_rank), generator=g, device=dev)
+                        / math.sqrt(wl.hidden)).to(tdt)
+        p0 = wl.prefill_lens[0]
+        posn = torch.arange(p0, p0 + wl.append_tokens)
+        d["slot"] = (table[0, posn // 64].long() * 64 + posn % 64).to(dev)
+    return d
+
+
+def algorithmic_bytes(wl):
+    """Bytes the method must move per step (see the design notes)."""
+    s = wl.elem_bytes
+    ctx = sum(wl.seq_lens)
+    latent = ctx * (wl.key_rank_total + wl.value_rank) * s
+    sizes = wl.group_sizes
+    factors = (sum(r * h * wl.head_dim for r, h in zip(wl.group_rank, sizes))
+               + wl.value_rank * wl.kv_dim) * s
+    qo = 2 * wl.batch * wl.num_q_heads * wl.head_dim * 4
+    append = 0
+    if wl.append_tokens:
+        R = wl.key_rank_total + wl.value_rank
+        append = (wl.append_tokens * wl.hidden + wl.hidden * R + wl.append_tokens * R) * s
+    return dict(latent=latent, factors=factors, q_out=qo, append=append,
+                decode_total=latent + factors + qo)
+
+
+def cpu_baseline(wl, budget_s):
+    """The oracle, as it stands, on a bounded sample of the same workload:
+    the append of all new tokens plus whole-context decode of as many heads
+    as fit the time budget; the step time is extrapolated to every head."""
+    import numpy as np
+    from oracle import append as oappend
+    from oracle import attention as oattn
+    from oracle.bookkeeping import book_for
+    from workloads.inputs import make_factors
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()
+                       if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    bk = book_for(wl)
+    g = np.random.default_rng(wl.seed)
+    L_keys, L_value, R_blocks, R_value = make_factors(wl)
+    b = 0
+    T = wl.seq_lens[b]
+    Zk = g.standard_normal((T, wl.key_rank_total), dtype=np.float32)
+    Zv = g.standard_normal((T, wl.value_rank), dtype=np.float32)
+    q = g.standard_normal((wl.batch, wl.num_q_heads, wl.head_dim))
+    t_app = 0.0
+    if wl.append_tokens:
+        x = g.standard_normal((wl.append_tokens, wl.hidden), dtype=np.float32)
+        t0 = time.perf_counter()
+        oappend.latents(x, L_keys, L_value, wl.dtype)
+        t_app = time.perf_counter() - t0
+    heads_done, t_dec = 0, 0.0
+    for h in range(wl.num_q_heads):
+        t0 = time.perf_counter()
+        oattn.decode_head(q[b, h], Zk, Zv, R_blocks, R_value, bk, h, chunk=16384)
+        t_dec += time.perf_counter() - t0
+        heads_done += 1
+        if t_dec + t_app >= budget_s:
+            break
+    rows = wl.batch * wl.num_q_heads
+    # every (sequence, head) row of a full step costs about T_b / T_0 of a sampled row
+    ctx_scale = sum(wl.seq_lens) / (wl.batch * T)
+    step_s = t_app + t_dec / heads_done * rows * ctx_scale
+    return {
+        "value": wl.batch / step_s,
+        "unit": "tokens/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"oracle append of {wl.append_tokens} tokens ({t_app:.2f} s) + fp64 decode of "
+                   f"{heads_done} of {rows} (sequence, head) rows at {T} context tokens "
+                   f"({t_dec:.2f} s), extrapolated to the full step ({step_s:.1f} s)"),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on exactly one GPU (got --gpus {args.gpus}); "
+              "the multi-GPU sharding is a design note only", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+    from paper_2607_24331_amd import Plan, decode, latent_append
+    from workloads import make_workload
+
+    wl = make_workload(args.workload)
+    plan = Plan(wl.hidden, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_of_kv,
+                wl.group_rank, wl.value_rank, wl.dtype, args.split_tokens)
+    inp = device_inputs(wl, plan, torch)
+    max_ctx = max(wl.seq_lens)
+    out = torch.empty((wl.batch, wl.num_q_heads, wl.head_dim), dtype=torch.float32, device="cuda")
+    ws = plan.new_workspace(wl.batch, max_ctx)
+
+    def step():
+        if wl.append_tokens:
+            latent_append(plan, inp["x"], inp["L_keys"], inp["L_value"], inp["slot"], inp["pool"])
+        decode(plan, inp["q"], inp["pool"], inp["page_table"], inp["seq_lens"], max_ctx,
+               inp["R_keys"], inp["R_value"], out=out, workspace=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] {wl.name}: warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+
+    K = args.steps
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    for a, b in ev:                        # create the underlying HIP events
+        a.record()
+        b.record()
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record()
+    for k in range(K):
+        plan.set_profile_events(*ev[k])
+        step()
+    t_end.record()
+    torch.cuda.synchronize()
+    plan.set_profile_events(None, None)
+    ms_total = t_start.elapsed_time(t_end)
+    ms_step = ms_total / K
+    kern_ms = sum(a.elapsed_time(b) for a, b in ev) / K
+    print(f"[bench] timed {K} steps: {ms_step:.4f} ms/step, split kernel {kern_ms:.4f} ms",
+          file=sys.stderr, flush=True)
+
+    nb = algorithmic_bytes(wl)
+    achieved = nb["latent"] / (kern_ms * 1e-3) / 1e9
+    value = wl.batch / (ms_step * 1e-3)
+    rec = {
+        "metric": "compressed-KV decode attention tokens/s (achieved HBM GB/s in roofline)",
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded random latents, factors, queries and new tokens of the workload's shapes)",
+        "config": {
+            "workload": wl.name,
+            "batch": wl.batch,
+            "context_tokens": sum(wl.seq_lens),
+            "appended_tokens": wl.append_tokens,
+            "q_heads": wl.num_q_heads, "kv_heads": wl.num_kv_heads, "head_dim": wl.head_dim,
+            "hidden": wl.hidden, "group_sizes": list(wl.group_sizes),
+            "group_ranks": list(wl.group_rank), "value_rank": wl.value_rank,
+            "latent_dtype": wl.dtype, "split_tokens": plan.split_tokens,
+        },
+        "context_tokens_per_s": sum(wl.seq_lens) / (ms_step * 1e-3),
+        "step_hbm_gbs": (nb["decode_total"] + nb["append"]) / (ms_step * 1e-3) / 1e9,
+        "roofline": {
+            "kernel": "split-K latent attention (split_valu)",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": None,
+            "kernel_ms": kern_ms,
+            "bytes_per_launch": nb["latent"],
+        },
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,193 @@
+/*
+ * dckv.h -- compressed-KV decode attention (DynaCalKV) on MI355X (gfx950).
+ *
+ * The method (Sec. III of the paper) caches, per token, low-rank latents
+ * instead of keys and values:
+ *   keys    the key projection W^(k) is split column-wise into groups of
+ *           heads; group g is factored W_g ~ L_g R_g with its own rank r_g
+ *           (Sec. III-C), so each token stores one r_g-wide latent per group;
+ *   values  the whole value projection is factored W^(v) ~ L_v R_v with one
+ *           rank r_v (Sec. III-D), so each token stores one r_v-wide latent
+ *           shared by every head;
+ *   write   z = x L (Sec. III-A) for new tokens;
+ *   read    x W ~ z R (Sec. III-A), used here without rebuilding keys or
+ *           values: each query head is folded into its group's latent space
+ *           (q_h R_{g,h}^T), scores are taken against the key latents, the
+ *           softmax-weighted sum is accumulated in value-latent space and
+ *           multiplied once by the head's slice of R_v.
+ *
+ * Conventions of this library (readings where the paper is silent):
+ *   - softmax scale 1/sqrt(d_h); no positional transform; no mask (a decode
+ *     query attends to every cached token of its sequence);
+ *   - query head h reads KV head floor(h / (H_q / H_kv));
+ *   - the heads of group g are ordered by ascending KV-head index: the j-th
+ *     of them owns columns [j*d_h, (j+1)*d_h) of R_g;
+ *   - group g's latent occupies key-latent columns [koff_g, koff_g + r_g),
+ *     koff_g = r_0 + ... + r_{g-1}.
+ *
+ * Paged cache layout (64 tokens per page; R_K = sum_g r_g; R_Kp = R_K
+ * rounded up to a multiple of 8; page_elems = 64*R_Kp + 64*r_v elements of
+ * the latent dtype):
+ *   key part    token-major [64][R_Kp]: (slot s, key column k) at s*R_Kp + k;
+ *               columns R_K..R_Kp-1 are written as zero by dckv_latent_append
+ *   value part  rank-major  [r_v][64]: (slot s, value column j) at
+ *               64*R_Kp + j*64 + s
+ *   Position pos of sequence b lives in page page_table[b*max_pages + pos/64],
+ *   slot pos%64.  Page p starts at element p*page_elems of the pool.
+ *
+ * Threading and ownership: the caller owns every device buffer (inputs,
+ * outputs, pool, workspace).  The library owns only the host-side plan.
+ * dckv_latent_append and dckv_decode enqueue kernels on the given HIP stream
+ * and return without synchronising; they allocate no device memory, copy
+ * nothing between host and device and never block.  All arguments are
+ * validated on the host before any launch: on failure the call returns a
+ * negative status, records a message for dckv_last_error and enqueues
+ * nothing.  Faults inside kernels surface at the caller's next
+ * synchronisation.  A plan may be shared by threads; the error message is
+ * per thread.
+ */
+#ifndef DCKV_H
+#define DCKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DCKV_PAGE_TOKENS 64
+#define DCKV_MAX_HEADS 64      /* H_q limit */
+#define DCKV_MAX_GROUPS 64     /* G limit */
+#define DCKV_MAX_HEAD_DIM 256  /* d_h limit */
+#define DCKV_MAX_VALUE_RANK 4096
+#define DCKV_MAX_GROUP_RANK 4096
+
+typedef enum {
+  DCKV_OK = 0,
+  DCKV_EINVAL = -1,      /* bad shape, partition, rank, pointer or size */
+  DCKV_EDTYPE = -2,      /* unsupported latent dtype */
+  DCKV_EALIGN = -3,      /* a device pointer is not 16-byte aligned */
+  DCKV_EWORKSPACE = -4,  /* workspace smaller than dckv_decode_workspace_bytes */
+  DCKV_EHIP = -5,        /* a HIP launch or query failed */
+  DCKV_ENOMEM = -6       /* host allocation for the plan failed */
+} dckv_status;
+
+typedef enum { DCKV_F32 = 0, DCKV_BF16 = 1 } dckv_dtype;
+
+/* One attention layer's compressed-KV description (host memory; copied by
+ * dckv_plan_create, so the arrays may be freed afterwards). */
+typedef struct dckv_layer_desc {
+  int32_t hidden;                  /* m: width of x (input of the K/V projections) */
+  int32_t num_q_heads;             /* H_q, 1..DCKV_MAX_HEADS, multiple of num_kv_heads */
+  int32_t num_kv_heads;            /* H_kv: the key/value heads the groups partition */
+  int32_t head_dim;                /* d_h, 1..DCKV_MAX_HEAD_DIM */
+  int32_t num_groups;              /* G, 1..DCKV_MAX_GROUPS */
+  const int32_t* group_of_kv_head; /* [H_kv] group id of each KV head; every group
+                                      must receive at least one head (Sec. III-C:
+                                      the group sizes sum to the head count) */
+  const int32_t* group_rank;       /* [G] r_g with 1 <= r_g <= min(m, h_g*d_h) */
+  int32_t value_rank;              /* r_v with 1 <= r_v <= min(m, H_kv*d_h) */
+  int32_t latent_dtype;            /* dckv_dtype of latents, x and the L/R factors */
+  int32_t split_tokens;            /* context tokens per decode work split; a
+                                      multiple of 64, or 0 for the default */
+} dckv_layer_desc;
+
+/* Derived layout facts of a plan. */
+typedef struct dckv_plan_geometry {
+  int32_t key_rank_total;          /* R_K = sum of r_g */
+  int32_t key_row_stride;          /* R_Kp: R_K rounded up to a multiple of 8 */
+  int32_t value_rank;              /* r_v */
+  int32_t q_per_kv;                /* H_q / H_kv */
+  int32_t folded_query_len;        /* sum over query heads h of r_{g(h)} */
+  int32_t split_tokens;            /* effective tokens per decode split */
+  int64_t page_elems;              /* elements per page: 64*R_Kp + 64*r_v */
+  int64_t value_base;              /* element offset of the value part in a page: 64*R_Kp */
+  int64_t key_factor_elems;        /* elements of the concatenated R_g blocks */
+} dckv_plan_geometry;
+
+typedef struct dckv_plan dckv_plan;  /* opaque, host memory only */
+
+/* Validate a layer description and build its plan (bookkeeping of Sec.
+ * III-C: the partition, head ratios, per-group column offsets).  Returns
+ * DCKV_EINVAL / DCKV_EDTYPE for invalid descriptions (*out untouched),
+ * DCKV_ENOMEM if the host allocation fails.  Makes no HIP call. */
+int dckv_plan_create(const dckv_layer_desc* desc, dckv_plan** out);
+
+/* Free a plan (NULL is accepted). */
+void dckv_plan_destroy(dckv_plan* plan);
+
+/* Copy the plan's bookkeeping out (host memory; any pointer may be NULL to
+ * skip that array):
+ *   geo           layout facts above
+ *   koff          [G]      koff_g, first key-latent column of group g
+ *   pos_in_group  [H_kv]   position of each KV head inside its group
+ *   qoff          [H_q+1]  offset of query head h's folded query
+ *                          (r_{g(h)} values) within one sequence's block
+ *   roff          [G+1]    element offset of R_g in the concatenated blocks
+ * Makes no HIP call. */
+int dckv_plan_info(const dckv_plan* plan, dckv_plan_geometry* geo, int32_t* koff,
+                   int32_t* pos_in_group, int32_t* qoff, int64_t* roff);
+
+/* Bytes of device workspace dckv_decode needs for `batch` sequences of at
+ * most `max_context` tokens.  Makes no HIP call. */
+int dckv_decode_workspace_bytes(const dckv_plan* plan, int32_t batch, int32_t max_context,
+                                size_t* bytes);
+
+/* Latent write for new tokens (Sec. III-A z = x L, per group L_g of Sec.
+ * III-C and whole-projection L_v of Sec. III-D), computed with fp32
+ * accumulation and rounded to nearest-even into the pool.
+ *   x        device [n_tok, m] row-major, latent dtype
+ *   L_keys   device [m, R_K] row-major = [L_0 | L_1 | ... | L_{G-1}]
+ *   L_value  device [m, r_v] row-major
+ *   slot     device int64 [n_tok]: page*64 + slot-in-page of each token;
+ *            a negative slot, or one at or beyond num_pages*64, skips the token
+ *   pool     device, num_pages * page_elems elements of the latent dtype
+ *   stream   hipStream_t (NULL: the null stream)
+ * n_tok == 0 is a no-op.  Pointers must be 16-byte aligned.  Two tokens
+ * with the same slot race (the last write is unspecified). */
+int dckv_latent_append(const dckv_plan* plan, const void* x, int32_t n_tok,
+                       const void* L_keys, const void* L_value, const int64_t* slot,
+                       void* pool, int64_t num_pages, void* stream);
+
+/* Decode attention for one query per sequence over the compressed cache.
+ *   q           device fp32 [batch, H_q, d_h]
+ *   pool        device, laid out as above (num_pages pages)
+ *   page_table  device int32 [batch, max_pages]; entries outside
+ *               [0, num_pages) are treated as empty pages (no fault, their
+ *               tokens contribute nothing)
+ *   seq_lens    device int32 [batch]; each is clamped to [0, max_context]
+ *   max_context host bound on every seq_len, at most max_pages*64
+ *   R_keys      device, the R_g blocks back to back, each [r_g, h_g*d_h]
+ *               row-major, group 0 first (key_factor_elems in total)
+ *   R_value     device [r_v, H_kv*d_h] row-major
+ *   out         device fp32 [batch, H_q, d_h]; a sequence of length 0 gets zeros
+ *   workspace   device scratch of at least dckv_decode_workspace_bytes(batch,
+ *               max_context) bytes, 256-byte aligned; its contents on entry
+ *               do not matter and are overwritten
+ * Results are bitwise reproducible for a fixed plan and inputs: the work
+ * split depends only on split_tokens and every reduction runs in a fixed
+ * order.  batch == 0 is a no-op. */
+int dckv_decode(const dckv_plan* plan, const float* q, int32_t batch, const void* pool,
+                int64_t num_pages, const int32_t* page_table, int32_t max_pages,
+                const int32_t* seq_lens, int32_t max_context, const void* R_keys,
+                const void* R_value, float* out, void* workspace, size_t workspace_bytes,
+                void* stream);
+
+/* Benchmark instrumentation (not part of the method).  With non-NULL
+ * hipEvent_t handles, every later dckv_decode on this plan records `before`
+ * on its stream immediately before the split-K attention kernel (the
+ * dominant kernel of a decode) and `after` immediately after it, so the
+ * caller can time that kernel alone; NULL handles switch this off.  The
+ * events stay owned by the caller.  A plan being instrumented must not be
+ * used by several threads at once.  Makes no HIP call itself. */
+int dckv_plan_set_profile_events(dckv_plan* plan, void* before, void* after);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char* dckv_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DCKV_H */

@@ -1,0 +1,224 @@
+// Decode attention over the compressed cache without rebuilding keys or
+// values (read side of Sec. III-A, x W ~ z R):
+//   fold   q~_h = q_h R_{g,h}^T * log2(e)/sqrt(d_h)   (Sec. III-C group factor)
+//   split  per (sequence, head, context split): scores s_t = q~_h . z_{g,t},
+//          online softmax in base 2, acc = sum_t p_t z_{v,t} in value-latent
+//          space (Sec. III-D shared value latent)
+//   merge  fixed ascending-split log-sum-exp merge, then o_h = (acc / l)
+//          R_v[:, kv(h) block] (one up-projection per head)
+#include <cmath>
+
+#include "device.h"
+#include "internal.h"
+
+namespace dckv {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kAccPerThread = DCKV_MAX_VALUE_RANK / kThreads;
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// ---------------------------------------------------------------- fold
+template <typename T>
+__global__ __launch_bounds__(kThreads) void fold_kernel(const float* __restrict__ q,
+                                                        const T* __restrict__ Rk,
+                                                        float* __restrict__ qt, HeadTables tb,
+                                                        float scale) {
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int dh = tb.head_dim;
+  __shared__ float qs[DCKV_MAX_HEAD_DIM];
+  for (int d = threadIdx.x; d < dh; d += kThreads) qs[d] = q[(int64_t(b) * tb.n_q_heads + h) * dh + d];
+  __syncthreads();
+  const int r = tb.rank_of_q[h];
+  const T* base = Rk + tb.roff_of_q[h] + tb.rcol_of_q[h];
+  const int stride = tb.rstride_of_q[h];
+  float* dst = qt + int64_t(b) * tb.qlen + tb.qoff[h];
+  for (int j = threadIdx.x; j < r; j += kThreads) {
+    const T* row = base + int64_t(j) * stride;
+    float acc = 0.f;
+    for (int d = 0; d < dh; ++d) acc = fmaf(qs[d], to_f32(row[d]), acc);
+    dst[j] = acc * scale;
+  }
+}
+
+// ------------------------------------------------- split (portable VALU)
+// One 256-thread block per (split, query head, sequence).  Scores: 4 threads
+// per token, each summing a quarter of the group's rank.  Values: each thread
+// owns value columns tid, tid+256, ...
+template <typename T>
+__global__ __launch_bounds__(kThreads) void split_valu(
+    const float* __restrict__ qt, const T* __restrict__ pool, int64_t num_pages,
+    const int32_t* __restrict__ page_table, int max_pages, const int32_t* __restrict__ seq_lens,
+    int max_context, int split_tokens, int n_split, int RKp, int rv, int64_t page_elems,
+    int64_t value_base, float* __restrict__ part_ml, float* __restrict__ part_acc, HeadTables tb) {
+  const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x;
+  __shared__ float qs[DCKV_MAX_GROUP_RANK];
+  __shared__ float part[4][DCKV_PAGE_TOKENS];
+  __shared__ float ps[DCKV_PAGE_TOKENS];
+
+  int T_b = seq_lens[b];
+  T_b = T_b < 0 ? 0 : (T_b > max_context ? max_context : T_b);
+  const int t0 = split * split_tokens;
+  const int t1 = min(t0 + split_tokens, T_b);
+  const int r = tb.rank_of_q[h];
+  const int koff = tb.koff_of_q[h];
+  for (int j = tid; j < r; j += kThreads) qs[j] = qt[int64_t(b) * tb.qlen + tb.qoff[h] + j];
+  __syncthreads();
+
+  float acc[kAccPerThread];
+#pragma unroll
+  for (int i = 0; i < kAccPerThread; ++i) acc[i] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+  const int slot = tid & (DCKV_PAGE_TOKENS - 1), quarter = tid >> 6;
+
+  for (int tok = t0; tok < t1; tok += DCKV_PAGE_TOKENS) {
+    const int n = min(DCKV_PAGE_TOKENS, t1 - tok);
+    const int page = page_table[int64_t(b) * max_pages + tok / DCKV_PAGE_TOKENS];
+    const bool valid = page >= 0 && page < num_pages;
+    const T* pg = pool + (valid ? int64_t(page) * page_elems : 0);
+    float sp = 0.f;
+    if (valid && slot < n) {
+      const T* krow = pg + int64_t(slot) * RKp + koff;
+      for (int k = quarter; k < r; k += 4) sp = fmaf(qs[k], to_f32(krow[k]), sp);
+    }
+    part[quarter][slot] = sp;
+    __syncthreads();
+    if (tid < DCKV_PAGE_TOKENS)
+      ps[tid] = (valid && tid < n) ? (part[0][tid] + part[1][tid]) + (part[2][tid] + part[3][tid])
+                                   : -INFINITY;
+    __syncthreads();
+    float cmax = -INFINITY;
+    for (int t = 0; t < n; ++t) cmax = fmaxf(cmax, ps[t]);
+    const float m_new = fmaxf(m_run, cmax);
+    __syncthreads();
+    if (m_new == -INFINITY) continue;  // uniform: no valid token so far
+    const float alpha = exp2f(m_run - m_new);
+    if (tid < DCKV_PAGE_TOKENS) ps[tid] = tid < n ? exp2f(ps[tid] - m_new) : 0.f;
+    __syncthreads();
+    float csum = 0.f;
+    for (int t = 0; t < n; ++t) csum += ps[t];
+    l_run = l_run * alpha + csum;
+#pragma unroll
+    for (int i = 0; i < kAccPerThread; ++i) {
+      const int j = tid + i * kThreads;
+      if (j < rv) {
+        float a = acc[i] * alpha;
+        if (valid) {
+          const T* vrow = pg + value_base + int64_t(j) * DCKV_PAGE_TOKENS;
+          for (int t = 0; t < n; ++t) a = fmaf(ps[t], to_f32(vrow[t]), a);
+        }
+        acc[i] = a;
+      }
+    }
+    m_run = m_new;
+    __syncthreads();
+  }
+
+  const int64_t row = (int64_t(b) * tb.n_q_heads + h) * n_split + split;
+  if (tid == 0) {
+    part_ml[row * 2 + 0] = m_run;
+    part_ml[row * 2 + 1] = l_run;
+  }
+#pragma unroll
+  for (int i = 0; i < kAccPerThread; ++i) {
+    const int j = tid + i * kThreads;
+    if (j < rv) part_acc[row * rv + j] = acc[i];
+  }
+}
+
+// ------------------------------------------------------ merge + up-project
+template <typename T>
+__global__ __launch_bounds__(kThreads) void merge_upproject(
+    const float* __restrict__ part_ml, const float* __restrict__ part_acc,
+    const T* __restrict__ Rv, float* __restrict__ out, int n_split, int rv, HeadTables tb) {
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int dh = tb.head_dim;
+  const int n = tb.n_kv_heads * dh;
+  const int kv = h / tb.q_per_kv;
+  __shared__ float ash[DCKV_MAX_VALUE_RANK];
+  const int64_t row0 = (int64_t(b) * tb.n_q_heads + h) * n_split;
+  float M = -INFINITY;
+  for (int s = 0; s < n_split; ++s) M = fmaxf(M, part_ml[(row0 + s) * 2]);
+  float* o = out + (int64_t(b) * tb.n_q_heads + h) * dh;
+  if (M == -INFINITY) {
+    for (int d = tid; d < dh; d += kThreads) o[d] = 0.f;
+    return;
+  }
+  float L = 0.f;
+  for (int s = 0; s < n_split; ++s) L += exp2f(part_ml[(row0 + s) * 2] - M) * part_ml[(row0 + s) * 2 + 1];
+  const float inv = 1.f / L;
+  for (int j = tid; j < rv; j += kThreads) {
+    float a = 0.f;
+    for (int s = 0; s < n_split; ++s) {
+      const float w = exp2f(part_ml[(row0 + s) * 2] - M);
+      a = fmaf(w, part_acc[(row0 + s) * rv + j], a);
+    }
+    ash[j] = a * inv;
+  }
+  __syncthreads();
+  for (int d = tid; d < dh; d += kThreads) {
+    float acc = 0.f;
+    const T* col = Rv + int64_t(kv) * dh + d;
+    for (int j = 0; j < rv; ++j) acc = fmaf(ash[j], to_f32(col[int64_t(j) * n]), acc);
+    o[d] = acc;
+  }
+}
+
+template <typename T>
+hipError_t launch_decode_t(const dckv_plan& p, const DecodeShape& sh, const float* q,
+                           const void* pool, int64_t num_pages, const int32_t* page_table,
+                           int32_t max_pages, const int32_t* seq_lens, const void* R_keys,
+                           const void* R_value, float* out, void* workspace, hipStream_t stream) {
+  char* ws = static_cast<char*>(workspace);
+  float* qt = reinterpret_cast<float*>(ws + sh.off_qt);
+  float* ml = reinterpret_cast<float*>(ws + sh.off_ml);
+  float* acc = reinterpret_cast<float*>(ws + sh.off_acc);
+  const float scale = kLog2e / std::sqrt(float(p.dh));
+  hipLaunchKernelGGL(fold_kernel<T>, dim3(p.Hq, sh.batch), dim3(kThreads), 0, stream, q,
+                     static_cast<const T*>(R_keys), qt, p.tables, scale);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (p.prof_before && (e = hipEventRecord(p.prof_before, stream)) != hipSuccess) return e;
+  hipLaunchKernelGGL(split_valu<T>, dim3(sh.n_split, p.Hq, sh.batch), dim3(kThreads), 0, stream, qt,
+                     static_cast<const T*>(pool), num_pages, page_table, max_pages, seq_lens,
+                     sh.max_context, sh.split_tokens, sh.n_split, p.RKp, p.rv, p.page_elems,
+                     p.value_base, ml, acc, p.tables);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (p.prof_after && (e = hipEventRecord(p.prof_after, stream)) != hipSuccess) return e;
+  hipLaunchKernelGGL(merge_upproject<T>, dim3(p.Hq, sh.batch), dim3(kThreads), 0, stream, ml, acc,
+                     static_cast<const T*>(R_value), out, sh.n_split, p.rv, p.tables);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+DecodeShape decode_shape(const dckv_plan& p, int32_t batch, int32_t max_context) {
+  DecodeShape s{};
+  s.batch = batch;
+  s.max_context = max_context;
+  s.split_tokens = p.split_tokens;
+  s.n_split = max_context > 0 ? (max_context + p.split_tokens - 1) / p.split_tokens : 1;
+  const size_t rows = size_t(batch) * p.Hq * s.n_split;
+  s.off_qt = 0;
+  s.off_ml = align_up(size_t(batch) * p.qlen * sizeof(float), 256);
+  s.off_acc = s.off_ml + align_up(rows * 2 * sizeof(float), 256);
+  s.bytes = s.off_acc + align_up(rows * p.rv * sizeof(float), 256);
+  return s;
+}
+
+hipError_t launch_decode(const dckv_plan& p, const DecodeShape& shape, const float* q,
+                         const void* pool, int64_t num_pages, const int32_t* page_table,
+                         int32_t max_pages, const int32_t* seq_lens, const void* R_keys,
+                         const void* R_value, float* out, void* workspace, hipStream_t stream) {
+  if (p.dtype == DCKV_F32)
+    return launch_decode_t<float>(p, shape, q, pool, num_pages, page_table, max_pages, seq_lens,
+                                  R_keys, R_value, out, workspace, stream);
+  return launch_decode_t<bf16>(p, shape, q, pool, num_pages, page_table, max_pages, seq_lens, R_keys,
+                               R_value, out, workspace, stream);
+}
+
+}  // namespace dckv

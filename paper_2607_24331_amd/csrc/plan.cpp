@@ -1,0 +1,238 @@
+// Host side of the C ABI: validation, the plan's bookkeeping (Sec. III-C
+// column-wise head groups with per-group ranks; Sec. III-D one value rank)
+// and argument checks before any kernel is enqueued.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <new>
+#include <string>
+
+#include "internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return status;
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+constexpr int32_t kDefaultSplitTokens = 1024;
+
+}  // namespace
+
+extern "C" {
+
+const char* dckv_last_error(void) { return g_last_error.c_str(); }
+
+int dckv_plan_create(const dckv_layer_desc* d, dckv_plan** out) {
+  if (!d || !out) return fail(DCKV_EINVAL, "plan_create: null desc or out pointer");
+  if (d->latent_dtype != DCKV_F32 && d->latent_dtype != DCKV_BF16)
+    return fail(DCKV_EDTYPE, "plan_create: latent_dtype %d is neither DCKV_F32 nor DCKV_BF16",
+                d->latent_dtype);
+  if (d->hidden < 1) return fail(DCKV_EINVAL, "plan_create: hidden %d < 1", d->hidden);
+  if (d->num_q_heads < 1 || d->num_q_heads > DCKV_MAX_HEADS)
+    return fail(DCKV_EINVAL, "plan_create: num_q_heads %d outside [1,%d]", d->num_q_heads,
+                DCKV_MAX_HEADS);
+  if (d->num_kv_heads < 1 || d->num_q_heads % d->num_kv_heads != 0)
+    return fail(DCKV_EINVAL, "plan_create: num_q_heads %d is not a multiple of num_kv_heads %d",
+                d->num_q_heads, d->num_kv_heads);
+  if (d->head_dim < 1 || d->head_dim > DCKV_MAX_HEAD_DIM)
+    return fail(DCKV_EINVAL, "plan_create: head_dim %d outside [1,%d]", d->head_dim,
+                DCKV_MAX_HEAD_DIM);
+  if (d->num_groups < 1 || d->num_groups > DCKV_MAX_GROUPS || d->num_groups > d->num_kv_heads)
+    return fail(DCKV_EINVAL, "plan_create: num_groups %d outside [1,min(%d,num_kv_heads)]",
+                d->num_groups, DCKV_MAX_GROUPS);
+  if (!d->group_of_kv_head || !d->group_rank)
+    return fail(DCKV_EINVAL, "plan_create: null group_of_kv_head or group_rank");
+  if (d->split_tokens < 0 || d->split_tokens % DCKV_PAGE_TOKENS != 0 || d->split_tokens > (1 << 24))
+    return fail(DCKV_EINVAL, "plan_create: split_tokens %d is not 0 or a positive multiple of %d",
+                d->split_tokens, DCKV_PAGE_TOKENS);
+
+  const int32_t Hkv = d->num_kv_heads, G = d->num_groups, dh = d->head_dim;
+  std::vector<int32_t> hg(G, 0), pos(Hkv, 0);
+  for (int32_t kv = 0; kv < Hkv; ++kv) {
+    const int32_t g = d->group_of_kv_head[kv];
+    if (g < 0 || g >= G)
+      return fail(DCKV_EINVAL, "plan_create: KV head %d assigned to group %d outside [0,%d)", kv, g, G);
+    pos[kv] = hg[g]++;  // ascending head order inside the group
+  }
+  for (int32_t g = 0; g < G; ++g) {
+    if (hg[g] == 0) return fail(DCKV_EINVAL, "plan_create: group %d has no heads", g);
+    const int64_t cap = std::min<int64_t>(d->hidden, int64_t(hg[g]) * dh);
+    const int32_t r = d->group_rank[g];
+    if (r < 1 || r > cap || r > DCKV_MAX_GROUP_RANK)
+      return fail(DCKV_EINVAL, "plan_create: rank %d of group %d outside [1,%lld] (limit %d)", r, g,
+                  (long long)cap, DCKV_MAX_GROUP_RANK);
+  }
+  const int64_t vcap = std::min<int64_t>(d->hidden, int64_t(Hkv) * dh);
+  if (d->value_rank < 1 || d->value_rank > vcap || d->value_rank > DCKV_MAX_VALUE_RANK)
+    return fail(DCKV_EINVAL, "plan_create: value_rank %d outside [1,%lld] (limit %d)", d->value_rank,
+                (long long)vcap, DCKV_MAX_VALUE_RANK);
+
+  dckv_plan* p = new (std::nothrow) dckv_plan();
+  if (!p) return fail(DCKV_ENOMEM, "plan_create: host allocation failed");
+  try {
+    p->m = d->hidden;
+    p->Hq = d->num_q_heads;
+    p->Hkv = Hkv;
+    p->dh = dh;
+    p->G = G;
+    p->rv = d->value_rank;
+    p->dtype = d->latent_dtype;
+    p->split_tokens = d->split_tokens ? d->split_tokens : kDefaultSplitTokens;
+    p->group_of_kv.assign(d->group_of_kv_head, d->group_of_kv_head + Hkv);
+    p->ranks.assign(d->group_rank, d->group_rank + G);
+    p->hg = hg;
+    p->pos_in_group = pos;
+    p->koff.resize(G);
+    p->roff.resize(G + 1);
+    int32_t acc = 0;
+    int64_t racc = 0;
+    for (int32_t g = 0; g < G; ++g) {
+      p->koff[g] = acc;
+      acc += p->ranks[g];
+      p->roff[g] = racc;
+      racc += int64_t(p->ranks[g]) * hg[g] * dh;
+    }
+    p->roff[G] = racc;
+    p->RK = acc;
+    p->RKp = (acc + 7) / 8 * 8;
+    p->key_factor_elems = racc;
+    p->page_elems = int64_t(DCKV_PAGE_TOKENS) * p->RKp + int64_t(DCKV_PAGE_TOKENS) * p->rv;
+    p->value_base = int64_t(DCKV_PAGE_TOKENS) * p->RKp;
+    p->qpk = p->Hq / Hkv;
+    p->qoff.resize(p->Hq + 1);
+    int32_t qacc = 0;
+    dckv::HeadTables& t = p->tables;
+    t = dckv::HeadTables{};
+    t.n_q_heads = p->Hq;
+    t.n_kv_heads = Hkv;
+    t.head_dim = dh;
+    t.q_per_kv = p->qpk;
+    t.n_groups = G;
+    for (int32_t h = 0; h < p->Hq; ++h) {
+      const int32_t kv = h / p->qpk, g = p->group_of_kv[kv];
+      p->qoff[h] = qacc;
+      t.qoff[h] = qacc;
+      t.rank_of_q[h] = p->ranks[g];
+      t.koff_of_q[h] = p->koff[g];
+      t.rcol_of_q[h] = pos[kv] * dh;
+      t.rstride_of_q[h] = hg[g] * dh;
+      t.roff_of_q[h] = p->roff[g];
+      qacc += p->ranks[g];
+    }
+    p->qoff[p->Hq] = qacc;
+    t.qoff[p->Hq] = qacc;
+    t.qlen = qacc;
+    p->qlen = qacc;
+  } catch (...) {
+    delete p;
+    return fail(DCKV_ENOMEM, "plan_create: host allocation failed");
+  }
+  *out = p;
+  return DCKV_OK;
+}
+
+void dckv_plan_destroy(dckv_plan* p) { delete p; }
+
+int dckv_plan_set_profile_events(dckv_plan* p, void* before, void* after) {
+  if (!p) return fail(DCKV_EINVAL, "plan_set_profile_events: null plan");
+  if ((before == nullptr) != (after == nullptr))
+    return fail(DCKV_EINVAL, "plan_set_profile_events: give both events or neither");
+  p->prof_before = static_cast<hipEvent_t>(before);
+  p->prof_after = static_cast<hipEvent_t>(after);
+  return DCKV_OK;
+}
+
+int dckv_plan_info(const dckv_plan* p, dckv_plan_geometry* geo, int32_t* koff,
+                   int32_t* pos_in_group, int32_t* qoff, int64_t* roff) {
+  if (!p) return fail(DCKV_EINVAL, "plan_info: null plan");
+  if (geo) {
+    geo->key_rank_total = p->RK;
+    geo->key_row_stride = p->RKp;
+    geo->value_rank = p->rv;
+    geo->q_per_kv = p->qpk;
+    geo->folded_query_len = p->qlen;
+    geo->split_tokens = p->split_tokens;
+    geo->page_elems = p->page_elems;
+    geo->value_base = p->value_base;
+    geo->key_factor_elems = p->key_factor_elems;
+  }
+  if (koff) std::copy(p->koff.begin(), p->koff.end(), koff);
+  if (pos_in_group) std::copy(p->pos_in_group.begin(), p->pos_in_group.end(), pos_in_group);
+  if (qoff) std::copy(p->qoff.begin(), p->qoff.end(), qoff);
+  if (roff) std::copy(p->roff.begin(), p->roff.end(), roff);
+  return DCKV_OK;
+}
+
+int dckv_decode_workspace_bytes(const dckv_plan* p, int32_t batch, int32_t max_context,
+                                size_t* bytes) {
+  if (!p || !bytes) return fail(DCKV_EINVAL, "decode_workspace_bytes: null plan or bytes pointer");
+  if (batch < 0 || max_context < 0)
+    return fail(DCKV_EINVAL, "decode_workspace_bytes: negative batch %d or max_context %d", batch,
+                max_context);
+  *bytes = dckv::decode_shape(*p, batch, max_context).bytes;
+  return DCKV_OK;
+}
+
+int dckv_latent_append(const dckv_plan* p, const void* x, int32_t n_tok, const void* L_keys,
+                       const void* L_value, const int64_t* slot, void* pool, int64_t num_pages,
+                       void* stream) {
+  if (!p) return fail(DCKV_EINVAL, "latent_append: null plan");
+  if (n_tok < 0) return fail(DCKV_EINVAL, "latent_append: n_tok %d < 0", n_tok);
+  if (n_tok == 0) return DCKV_OK;
+  if (!x || !L_keys || !L_value || !slot || !pool)
+    return fail(DCKV_EINVAL, "latent_append: null device pointer");
+  if (num_pages < 1) return fail(DCKV_EINVAL, "latent_append: num_pages %lld < 1", (long long)num_pages);
+  if (n_tok > 64 * 65535) return fail(DCKV_EINVAL, "latent_append: n_tok %d above %d", n_tok, 64 * 65535);
+  if (!aligned(x, 16) || !aligned(L_keys, 16) || !aligned(L_value, 16) || !aligned(pool, 16) ||
+      !aligned(slot, 8))
+    return fail(DCKV_EALIGN, "latent_append: x, L_keys, L_value and pool must be 16-byte aligned, slot 8-byte");
+  hipError_t e = dckv::launch_append(*p, x, n_tok, L_keys, L_value, slot, pool, num_pages,
+                                     static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(DCKV_EHIP, "latent_append: %s", hipGetErrorString(e));
+  return DCKV_OK;
+}
+
+int dckv_decode(const dckv_plan* p, const float* q, int32_t batch, const void* pool,
+                int64_t num_pages, const int32_t* page_table, int32_t max_pages,
+                const int32_t* seq_lens, int32_t max_context, const void* R_keys,
+                const void* R_value, float* out, void* workspace, size_t workspace_bytes,
+                void* stream) {
+  if (!p) return fail(DCKV_EINVAL, "decode: null plan");
+  if (batch < 0) return fail(DCKV_EINVAL, "decode: batch %d < 0", batch);
+  if (batch == 0) return DCKV_OK;
+  if (!q || !pool || !page_table || !seq_lens || !R_keys || !R_value || !out || !workspace)
+    return fail(DCKV_EINVAL, "decode: null device pointer");
+  if (batch > 65535) return fail(DCKV_EINVAL, "decode: batch %d above 65535", batch);
+  if (num_pages < 1) return fail(DCKV_EINVAL, "decode: num_pages %lld < 1", (long long)num_pages);
+  if (max_pages < 1) return fail(DCKV_EINVAL, "decode: max_pages %d < 1", max_pages);
+  if (max_context < 0 || int64_t(max_context) > int64_t(max_pages) * DCKV_PAGE_TOKENS)
+    return fail(DCKV_EINVAL, "decode: max_context %d outside [0, max_pages*64 = %lld]", max_context,
+                (long long)max_pages * DCKV_PAGE_TOKENS);
+  if (!aligned(q, 16) || !aligned(pool, 16) || !aligned(R_keys, 16) || !aligned(R_value, 16) ||
+      !aligned(out, 16) || !aligned(page_table, 4) || !aligned(seq_lens, 4))
+    return fail(DCKV_EALIGN, "decode: q, pool, R_keys, R_value and out must be 16-byte aligned");
+  if (!aligned(workspace, 256)) return fail(DCKV_EALIGN, "decode: workspace must be 256-byte aligned");
+  const dckv::DecodeShape shape = dckv::decode_shape(*p, batch, max_context);
+  if (workspace_bytes < shape.bytes)
+    return fail(DCKV_EWORKSPACE, "decode: workspace of %zu bytes, %zu needed", workspace_bytes,
+                shape.bytes);
+  hipError_t e = dckv::launch_decode(*p, shape, q, pool, num_pages, page_table, max_pages, seq_lens,
+                                     R_keys, R_value, out, workspace, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(DCKV_EHIP, "decode: %s", hipGetErrorString(e));
+  return DCKV_OK;
+}
+
+}  // extern "C"

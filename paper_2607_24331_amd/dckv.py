@@ -1,0 +1,190 @@
+"""Python binding of libdckv (argument marshalling only).
+
+Every step of append and decode runs in the HIP kernels behind the C ABI;
+PyTorch supplies device memory and the current stream.  The functions take
+torch tensors on the GPU, check their dtypes, shapes and contiguity against
+the plan, and pass raw pointers down.
+"""
+
+from __future__ import annotations
+
+import ctypes
+from typing import Optional, Sequence
+
+import torch
+
+from . import capi
+
+_lib = capi.load()
+
+_DTYPES = {"f32": (capi.DCKV_F32, torch.float32), "bf16": (capi.DCKV_BF16, torch.bfloat16)}
+
+
+class DckvError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        msg = _lib.dckv_last_error().decode(errors="replace")
+        super().__init__(f"{where}: {capi.STATUS_NAMES.get(status, status)}: {msg}")
+
+
+def _check(status: int, where: str) -> None:
+    if status != capi.DCKV_OK:
+        raise DckvError(status, where)
+
+
+def _i32_array(values: Sequence[int]):
+    arr = (ctypes.c_int32 * len(values))(*[int(v) for v in values])
+    return arr
+
+
+class Plan:
+    """Host plan of one layer: grouping, ranks, layout and split size."""
+
+    def __init__(self, hidden: int, num_q_heads: int, num_kv_heads: int, head_dim: int,
+                 group_of_kv_head: Sequence[int], group_rank: Sequence[int], value_rank: int,
+                 dtype: str = "bf16", split_tokens: int = 0):
+        if dtype not in _DTYPES:
+            raise ValueError(f"dtype must be one of {sorted(_DTYPES)}")
+        self.dtype = dtype
+        self.torch_dtype = _DTYPES[dtype][1]
+        self._gmap = _i32_array(group_of_kv_head)
+        self._ranks = _i32_array(group_rank)
+        desc = capi.LayerDesc(hidden, num_q_heads, num_kv_heads, head_dim, len(group_rank),
+                              ctypes.cast(self._gmap, ctypes.POINTER(ctypes.c_int32)),
+                              ctypes.cast(self._ranks, ctypes.POINTER(ctypes.c_int32)),
+                              value_rank, _DTYPES[dtype][0], split_tokens)
+        handle = ctypes.c_void_p()
+        _check(_lib.dckv_plan_create(ctypes.byref(desc), ctypes.byref(handle)), "plan_create")
+        self._handle = handle
+        self.hidden, self.num_q_heads, self.num_kv_heads = hidden, num_q_heads, num_kv_heads
+        self.head_dim, self.num_groups, self.value_rank = head_dim, len(group_rank), value_rank
+        info = self.info()
+        self.geometry = info["geometry"]
+        self.key_rank_total = self.geometry["key_rank_total"]
+        self.key_row_stride = self.geometry["key_row_stride"]
+        self.page_elems = self.geometry["page_elems"]
+        self.split_tokens = self.geometry["split_tokens"]
+        self.key_factor_elems = self.geometry["key_factor_elems"]
+
+    @property
+    def handle(self) -> ctypes.c_void_p:
+        if self._handle is None:
+            raise ValueError("plan is closed")
+        return self._handle
+
+    def info(self) -> dict:
+        geo = capi.PlanGeometry()
+        G, Hkv, Hq = self.num_groups, self.num_kv_heads, self.num_q_heads
+        koff = (ctypes.c_int32 * G)()
+        pos = (ctypes.c_int32 * Hkv)()
+        qoff = (ctypes.c_int32 * (Hq + 1))()
+        roff = (ctypes.c_int64 * (G + 1))()
+        _check(_lib.dckv_plan_info(self.handle, ctypes.byref(geo), koff, pos, qoff, roff), "plan_info")
+        return {
+            "geometry": {name: getattr(geo, name) for name, _ in capi.PlanGeometry._fields_},
+            "koff": list(koff), "pos_in_group": list(pos), "qoff": list(qoff), "roff": list(roff),
+        }
+
+    def workspace_bytes(self, batch: int, max_context: int) -> int:
+        n = ctypes.c_size_t()
+        _check(_lib.dckv_decode_workspace_bytes(self.handle, batch, max_context, ctypes.byref(n)),
+               "decode_workspace_bytes")
+        return n.value
+
+    def new_pool(self, num_pages: int, device="cuda") -> torch.Tensor:
+        """Zero-filled pool of `num_pages` pages."""
+        return torch.zeros((num_pages, self.page_elems), dtype=self.torch_dtype, device=device)
+
+    def new_workspace(self, batch: int, max_context: int, device="cuda") -> torch.Tensor:
+        n = self.workspace_bytes(batch, max_context)
+        return torch.empty(max(n, 256), dtype=torch.uint8, device=device)
+
+    def set_profile_events(self, before=None, after=None) -> None:
+        """Record two torch.cuda.Event objects around the split-K attention
+        kernel of every later decode (benchmark instrumentation); None stops."""
+        hb = before.cuda_event if before is not None else None
+        ha = after.cuda_event if after is not None else None
+        _check(_lib.dckv_plan_set_profile_events(self.handle, hb, ha), "plan_set_profile_events")
+
+    def close(self) -> None:
+        if getattr(self, "_handle", None) is not None:
+            _lib.dckv_plan_destroy(self._handle)
+            self._handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _stream_handle(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def _dev(t: torch.Tensor, name: str, dtype, shape=None) -> int:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on the GPU")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return t.data_ptr()
+
+
+def _num_pages(plan: Plan, pool: torch.Tensor) -> int:
+    if pool.numel() % plan.page_elems:
+        raise ValueError("pool size is not a whole number of pages")
+    return pool.numel() // plan.page_elems
+
+
+def latent_append(plan: Plan, x: torch.Tensor, L_keys: torch.Tensor, L_value: torch.Tensor,
+                  slot: torch.Tensor, pool: torch.Tensor, stream=None) -> None:
+    """Write z = x [L_keys | L_value] of each row of x into its pool slot."""
+    n_tok = x.shape[0] if x.dim() == 2 else -1
+    dt = plan.torch_dtype
+    px = _dev(x, "x", dt, (n_tok, plan.hidden))
+    pk = _dev(L_keys, "L_keys", dt, (plan.hidden, plan.key_rank_total))
+    pv = _dev(L_value, "L_value", dt, (plan.hidden, plan.value_rank))
+    ps = _dev(slot, "slot", torch.int64, (n_tok,))
+    pp = _dev(pool, "pool", dt)
+    _check(_lib.dckv_latent_append(plan.handle, px, n_tok, pk, pv, ps, pp, _num_pages(plan, pool),
+                                   _stream_handle(stream)), "latent_append")
+
+
+def decode(plan: Plan, q: torch.Tensor, pool: torch.Tensor, page_table: torch.Tensor,
+           seq_lens: torch.Tensor, max_context: int, R_keys: torch.Tensor, R_value: torch.Tensor,
+           out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+           stream=None) -> torch.Tensor:
+    """Attention output [batch, H_q, d_h] (fp32) of one query per sequence."""
+    if q.dim() != 3:
+        raise ValueError("q must be [batch, H_q, d_h]")
+    B = q.shape[0]
+    dt = plan.torch_dtype
+    pq = _dev(q, "q", torch.float32, (B, plan.num_q_heads, plan.head_dim))
+    pp = _dev(pool, "pool", dt)
+    if page_table.dim() != 2 or page_table.shape[0] != B:
+        raise ValueError("page_table must be [batch, max_pages]")
+    pt = _dev(page_table, "page_table", torch.int32)
+    psl = _dev(seq_lens, "seq_lens", torch.int32, (B,))
+    prk = _dev(R_keys, "R_keys", dt)
+    if R_keys.numel() != plan.key_factor_elems:
+        raise ValueError(f"R_keys holds {R_keys.numel()} elements, expected {plan.key_factor_elems}")
+    prv = _dev(R_value, "R_value", dt, (plan.value_rank, plan.num_kv_heads * plan.head_dim))
+    if out is None:
+        out = torch.empty((B, plan.num_q_heads, plan.head_dim), dtype=torch.float32, device=q.device)
+    po = _dev(out, "out", torch.float32, (B, plan.num_q_heads, plan.head_dim))
+    need = plan.workspace_bytes(B, max_context)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=q.device)
+    pw = _dev(workspace, "workspace", torch.uint8)
+    _check(_lib.dckv_decode(plan.handle, pq, B, pp, _num_pages(plan, pool), pt, page_table.shape[1],
+                            psl, int(max_context), prk, prv, po, pw, workspace.numel(),
+                            _stream_handle(stream)), "decode")
+    return out

@@ -1,0 +1,271 @@
+"""GPU parity of latent_append and decode against the CPU oracle.
+
+Small cases compare every output row and span several page tiles, splits,
+ragged tails, singleton groups, odd ranks, GQA and permuted pages; the
+full-size workloads compare sampled rows the oracle computes one by one.
+Tolerances: attention rows within 2e-2 relative (bf16 latents, fp32
+accumulation), 1e-4 for fp32 latents; latent writes bit-exact on
+exact-arithmetic inputs and otherwise within one bf16 ulp plus the fp32
+accumulation bound.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import append as oappend
+from oracle import attention as oattn
+from oracle import bf16 as obf16
+from oracle import layout as olayout
+from oracle.bookkeeping import book_for
+from workloads import WORKLOAD_NAMES, make_workload
+from workloads.configs import custom_workload
+from workloads.inputs import bf16_bits_from_f32, make_inputs
+
+from gpu_common import (TOL_REL_ROW, TOL_REL_ROW_F32, dev, gpu_pool_with_append, oracle_pool,
+                        oracle_rows, plan_for, row_rel_err, run_decode, sample_pairs, append_slots)
+
+pytestmark = pytest.mark.gpu
+
+
+def _report(name, errs):
+    print(f"[parity] {name}: max row rel err {max(errs):.3e} over {len(errs)} rows", flush=True)
+
+
+def _groups(sizes, seed):
+    g = np.random.default_rng(seed)
+    perm = g.permutation(sum(sizes))
+    gmap = [0] * sum(sizes)
+    pos = 0
+    for grp, s in enumerate(sizes):
+        for h in perm[pos:pos + s]:
+            gmap[int(h)] = grp
+        pos += s
+    return tuple(gmap)
+
+
+SMALL = {
+    # MHA with a singleton, odd ranks, a 1-token and an empty sequence, shuffled pages
+    "mha_odd": dict(hidden=256, num_q_heads=8, num_kv_heads=8, head_dim=64, sizes=(1, 3, 4),
+                    group_rank=(37, 101, 129), value_rank=96, seq_lens=(300, 64, 1, 0, 129),
+                    permute_pages=True, split=128),
+    # GQA 4 queries per KV head, uneven groups
+    "gqa_uneven": dict(hidden=512, num_q_heads=16, num_kv_heads=4, head_dim=128, sizes=(2, 1, 1),
+                       group_rank=(200, 77, 128), value_rank=256, seq_lens=(1000, 777),
+                       permute_pages=False, split=256),
+    # one group holding every head, value rank not a multiple of 64
+    "single_group": dict(hidden=384, num_q_heads=4, num_kv_heads=4, head_dim=64, sizes=(4,),
+                         group_rank=(160,), value_rank=200, seq_lens=(517,), permute_pages=True,
+                         split=64),
+    # many singletons (as the grouping often yields), d_h 128
+    "singletons": dict(hidden=1024, num_q_heads=8, num_kv_heads=8, head_dim=128,
+                       sizes=(1, 1, 1, 2, 1, 1, 1), group_rank=(31, 64, 17, 150, 99, 128, 5),
+                       value_rank=384, seq_lens=(2049, 65, 640), permute_pages=True, split=512),
+}
+
+
+def _small_inputs(name, dtype="bf16"):
+    c = SMALL[name]
+    wl = custom_workload(name=name, seed=100 + list(SMALL).index(name), hidden=c["hidden"],
+                         num_q_heads=c["num_q_heads"], num_kv_heads=c["num_kv_heads"],
+                         head_dim=c["head_dim"], group_of_kv=_groups(c["sizes"], 7),
+                         group_rank=c["group_rank"], value_rank=c["value_rank"], dtype=dtype,
+                         batch=len(c["seq_lens"]), seq_lens=c["seq_lens"],
+                         prefill_lens=c["seq_lens"], factor_scheme="orthonormal",
+                         permute_pages=c["permute_pages"])
+    return wl, make_inputs(wl), c["split"]
+
+
+def _all_rows(inp, q=None):
+    wl = inp.wl
+    pairs = [(b, h) for b in range(wl.batch) for h in range(wl.num_q_heads)]
+    return oracle_rows(inp, pairs, q=q)
+
+
+# ------------------------------------------------------------------ tiny fp32
+def test_tiny_mha_f32_append_then_decode():
+    wl = make_workload("tiny_mha_f32")
+    inp = make_inputs(wl)
+    plan = plan_for(wl)
+    pool = gpu_pool_with_append(inp, plan)
+    got_pool = pool.cpu().numpy()
+    # append: every latent within fp32 rounding of the exact product
+    Zk_g, Zv_g = olayout.unpack(got_pool, inp.page_table, 0, 256, wl.key_rank_total, wl.value_rank)
+    for Zg, L in ((Zk_g, inp.L_keys), (Zv_g, inp.L_value)):
+        exact = oappend.down_project(inp.x, L)
+        bound = wl.hidden * 2.0 ** -24 * oappend.abs_bound(inp.x, L) + np.abs(exact) * 2.0 ** -23
+        assert np.all(np.abs(Zg - exact) <= bound)
+    out = run_decode(inp, plan, pool)
+    ref_pool = oracle_pool(inp)
+    ref = oattn.decode(inp.q, ref_pool, inp.page_table, wl.seq_lens, inp.R_blocks, inp.R_value,
+                       book_for(wl), chunk=None)
+    errs = [row_rel_err(out[0, h], ref[0, h]) for h in range(wl.num_q_heads)]
+    _report("tiny_mha_f32", errs)
+    assert max(errs) <= TOL_REL_ROW_F32
+
+
+# ------------------------------------------------------------------ small bf16
+@pytest.mark.parametrize("name", list(SMALL))
+def test_small_decode_all_rows(name):
+    wl, inp, split = _small_inputs(name)
+    plan = plan_for(wl, split)
+    pool = gpu_pool_with_append(inp, plan)
+    out = run_decode(inp, plan, pool)
+    ref = _all_rows(inp)
+    errs = []
+    for (b, h), o in ref.items():
+        if wl.seq_lens[b] == 0:
+            assert np.all(out[b, h] == 0)
+            continue
+        errs.append(row_rel_err(out[b, h], o))
+    _report(name, errs)
+    assert max(errs) <= TOL_REL_ROW
+
+
+def test_peaked_softmax():
+    wl, inp, split = _small_inputs("gqa_uneven")
+    plan = plan_for(wl, split)
+    pool = gpu_pool_with_append(inp, plan)
+    q = inp.q * 16.0
+    out = run_decode(inp, plan, pool, q=q)
+    ref = _all_rows(inp, q=q)
+    errs = [row_rel_err(out[b, h], o) for (b, h), o in ref.items()]
+    _report("peaked", errs)
+    assert max(errs) <= TOL_REL_ROW
+
+
+def test_split_invariance_and_determinism():
+    wl, inp, _ = _small_inputs("singletons")
+    outs = []
+    for split in (64, 192, 1024, 4096):
+        plan = plan_for(wl, split)
+        pool = gpu_pool_with_append(inp, plan)
+        a = run_decode(inp, plan, pool)
+        b = run_decode(inp, plan, pool)
+        assert np.array_equal(a, b)                       # bitwise repeatable
+        outs.append(a)
+    for o in outs[1:]:
+        assert np.max(np.abs(o - outs[0])) <= 1e-3 * np.max(np.abs(outs[0]))
+
+
+def test_physical_page_permutation_is_invisible():
+    wl, inp, split = _small_inputs("mha_odd")
+    plan = plan_for(wl, split)
+    pool = gpu_pool_with_append(inp, plan)
+    out = run_decode(inp, plan, pool)
+    # move every page to a new physical place and rewrite the table
+    g = np.random.default_rng(3)
+    perm = g.permutation(inp.num_pages)
+    pool2 = torch.empty_like(pool)
+    pool2[torch.from_numpy(perm).cuda()] = pool
+    table2 = perm[inp.page_table].astype(np.int32)
+    inp.page_table = table2
+    out2 = run_decode(inp, plan, pool2)
+    assert np.array_equal(out, out2)
+
+
+def test_out_of_range_pages_are_skipped_without_fault():
+    wl, inp, split = _small_inputs("gqa_uneven")
+    plan = plan_for(wl, split)
+    pool = gpu_pool_with_append(inp, plan)
+    inp.page_table = inp.page_table.copy()
+    inp.page_table[1, 3] = inp.num_pages + 5      # invalid entry inside sequence 1
+    out = run_decode(inp, plan, pool)
+    assert np.isfinite(out).all()
+
+
+# --------------------------------------------------------------- append checks
+def test_append_layout_bit_exact_on_exact_inputs():
+    # Small-integer x and L: every product and sum is exact in fp32 and bf16,
+    # so the pool must equal the oracle's packing bit for bit, including the
+    # zero padding columns and the untouched slots.
+    wl, inp, split = _small_inputs("singletons")
+    g = np.random.default_rng(9)
+    n = 150
+    x = g.integers(-2, 3, size=(n, wl.hidden)).astype(np.float32) * (g.random((n, wl.hidden)) < 0.02)
+    Lk = g.integers(-2, 3, size=(wl.hidden, wl.key_rank_total)).astype(np.float32)
+    Lv = g.integers(-2, 3, size=(wl.hidden, wl.value_rank)).astype(np.float32)
+    pages = 5
+    table = np.array([[4, 0, 2]], dtype=np.int32)
+    start = 37
+    pos = start + np.arange(n)
+    slots = table[0, pos // 64].astype(np.int64) * 64 + pos % 64
+    sentinel = np.float32(-7.0)
+    ref = np.full((pages, olayout.page_elems(wl.key_rank_total, wl.value_rank)), sentinel, np.float32)
+    oappend.append(ref, table, 0, start, x, Lk, Lv, "bf16")
+    # the oracle's packing writes the padding columns of written rows as zero
+    RK, RKp = wl.key_rank_total, olayout.key_row_stride(wl.key_rank_total)
+    for p in pos:
+        ref[table[0, p // 64], (p % 64) * RKp + RK:(p % 64) * RKp + RKp] = 0
+    plan = plan_for(wl, split)
+    from paper_2607_24331_amd import latent_append
+    pool = dev(np.full(ref.shape, sentinel, np.float32), "bf16")
+    latent_append(plan, dev(x, "bf16"), dev(Lk, "bf16"), dev(Lv, "bf16"),
+                  torch.from_numpy(slots).cuda(), pool)
+    torch.cuda.synchronize()
+    got_bits = pool.view(torch.int16).cpu().numpy().view(np.uint16)
+    assert np.array_equal(got_bits, bf16_bits_from_f32(ref.astype(np.float32)))
+
+
+def test_append_random_within_one_ulp():
+    wl, inp, split = _small_inputs("gqa_uneven")
+    g = np.random.default_rng(1)
+    n = 333
+    from workloads.inputs import to_storage
+    x = to_storage(g.standard_normal((n, wl.hidden)), "bf16")
+    Lk = to_storage(g.standard_normal((wl.hidden, wl.key_rank_total)) / np.sqrt(wl.hidden), "bf16")
+    Lv = to_storage(g.standard_normal((wl.hidden, wl.value_rank)) / np.sqrt(wl.hidden), "bf16")
+    table = np.arange(6, dtype=np.int32)[None, :]
+    slots = np.arange(n, dtype=np.int64)
+    slots[5] = -1                       # skipped token
+    plan = plan_for(wl, split)
+    from paper_2607_24331_amd import latent_append
+    pool = plan.new_pool(6)
+    latent_append(plan, dev(x, "bf16"), dev(Lk, "bf16"), dev(Lv, "bf16"),
+                  torch.from_numpy(slots).cuda(), pool)
+    torch.cuda.synchronize()
+    Zk_g, Zv_g = olayout.unpack(pool.float().cpu().numpy(), table, 0, n, wl.key_rank_total, wl.value_rank)
+    for Zg, L in ((Zk_g, Lk), (Zv_g, Lv)):
+        exact = oappend.down_project(x, L)
+        rounded = obf16.round_to_bf16(exact)
+        bound = obf16.ulp_bf16(rounded) + wl.hidden * 2.0 ** -24 * oappend.abs_bound(x, L)
+        diff = np.abs(Zg - rounded)
+        keep = np.ones(n, bool)
+        keep[5] = False
+        assert np.all(diff[keep] <= bound[keep])
+        assert np.mean(Zg[keep] == rounded[keep]) > 0.99
+        assert np.all(Zg[5] == 0)        # skipped slot untouched
+
+
+# ------------------------------------------------------------ full workloads
+@pytest.mark.parametrize("name", [n for n in WORKLOAD_NAMES if n != "tiny_mha_f32"])
+def test_full_workload_sampled_rows(name):
+    wl = make_workload(name)
+    print(f"[parity] start {name}", flush=True)
+    inp = make_inputs(wl)
+    plan = plan_for(wl)
+    pool = gpu_pool_with_append(inp, plan)
+    out = run_decode(inp, plan, pool)
+    assert np.isfinite(out).all()
+    out2 = run_decode(inp, plan, pool)
+    assert np.array_equal(out, out2)
+    if wl.append_tokens:
+        # the appended latents, read back through the oracle's layout
+        RK, rv = wl.key_rank_total, wl.value_rank
+        first = wl.prefill_lens[0] // 64
+        last = -(-wl.seq_lens[0] // 64)
+        pages = torch.from_numpy(inp.page_table[0, first:last].astype(np.int64)).cuda()
+        part = pool[pages].float().cpu().numpy()
+        tbl = np.arange(part.shape[0], dtype=np.int32)[None, :]
+        skip = wl.prefill_lens[0] % 64
+        Zk_g, Zv_g = olayout.unpack(part, tbl, 0, skip + wl.append_tokens, RK, rv)
+        for Zg, L in ((Zk_g[skip:], inp.L_keys), (Zv_g[skip:], inp.L_value)):
+            exact = oappend.down_project(inp.x, L)
+            rounded = obf16.round_to_bf16(exact)
+            bound = obf16.ulp_bf16(rounded) + wl.hidden * 2.0 ** -24 * oappend.abs_bound(inp.x, L)
+            assert np.all(np.abs(Zg - rounded) <= bound)
+    pairs = sample_pairs(wl, 8 if wl.seq_lens[0] < 100000 else 5)
+    ref = oracle_rows(inp, pairs)
+    errs = [row_rel_err(out[b, h], ref[(b, h)]) for b, h in pairs]
+    _report(name, errs)
+    assert max(errs) <= TOL_REL_ROW

@@ -1,0 +1,162 @@
+"""Host-side checks of libdckv: exported symbols, plan bookkeeping against the
+oracle's independent bookkeeping (bit-exact), and validation errors.  Nothing
+here launches a kernel."""
+
+import ctypes
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import layout as olayout
+from oracle.bookkeeping import book_for, make_book
+from workloads import WORKLOAD_NAMES, make_workload
+
+capi = pytest.importorskip("paper_2607_24331_amd.capi")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return capi.load()
+
+
+def test_every_declared_function_is_exported(lib):
+    names = capi.header_functions()
+    assert set(names) == set(capi.SIGNATURES), names
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def _plan(wl, split_tokens=0):
+    from paper_2607_24331_amd import Plan
+    return Plan(wl.hidden, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_of_kv,
+                wl.group_rank, wl.value_rank, wl.dtype, split_tokens)
+
+
+@pytest.mark.parametrize("name", WORKLOAD_NAMES)
+def test_bookkeeping_matches_oracle(name):
+    wl = make_workload(name)
+    bk = book_for(wl)
+    info = _plan(wl).info()
+    geo = info["geometry"]
+    assert info["koff"] == bk.koff
+    assert info["pos_in_group"] == bk.pos_in_group
+    assert info["qoff"] == bk.qoff
+    assert info["roff"] == bk.roff
+    assert geo["key_rank_total"] == bk.key_rank_total
+    assert geo["key_row_stride"] == olayout.key_row_stride(bk.key_rank_total)
+    assert geo["page_elems"] == olayout.page_elems(bk.key_rank_total, bk.value_rank)
+    assert geo["value_base"] == olayout.value_base(bk.key_rank_total)
+    assert geo["q_per_kv"] == bk.q_per_kv
+    assert geo["folded_query_len"] == bk.qoff[-1]
+    assert geo["key_factor_elems"] == bk.roff[-1]
+
+
+def test_bookkeeping_random_layers():
+    from paper_2607_24331_amd import Plan
+    g = np.random.default_rng(5)
+    for _ in range(200):
+        Hkv = int(g.integers(1, 17))
+        qpk = int(g.choice([1, 2, 4]))
+        if Hkv * qpk > 64:
+            continue
+        d = int(g.choice([8, 64, 128]))
+        G = int(g.integers(1, Hkv + 1))
+        gmap = list(g.permutation(np.concatenate([np.arange(G), g.integers(0, G, Hkv - G)])))
+        m = int(g.integers(64, 5000))
+        sizes = [gmap.count(i) for i in range(G)]
+        ranks = [int(g.integers(1, min(m, s * d) + 1)) for s in sizes]
+        rv = int(g.integers(1, min(m, Hkv * d, 4096) + 1))
+        if max(ranks) > 4096:
+            continue
+        bk = make_book(m, Hkv * qpk, Hkv, d, gmap, ranks, rv)
+        info = Plan(m, Hkv * qpk, Hkv, d, gmap, ranks, rv, "bf16").info()
+        assert (info["koff"], info["pos_in_group"], info["qoff"], info["roff"]) == \
+            (bk.koff, bk.pos_in_group, bk.qoff, bk.roff)
+
+
+@pytest.mark.parametrize("change, status", [
+    (dict(gmap=[0, 0, 0, 0]), "DCKV_EINVAL"),            # group 1 empty
+    (dict(gmap=[0, 1, 2, 1]), "DCKV_EINVAL"),            # group id out of range
+    (dict(ranks=[0, 8]), "DCKV_EINVAL"),
+    (dict(ranks=[33, 8]), "DCKV_EINVAL"),                # above h_g * d_h = 32
+    (dict(num_q=6), "DCKV_EINVAL"),
+    (dict(value_rank=65), "DCKV_EINVAL"),
+    (dict(dtype=7), "DCKV_EDTYPE"),
+    (dict(split=100), "DCKV_EINVAL"),
+    (dict(head_dim=300), "DCKV_EINVAL"),
+])
+def test_plan_create_rejects(lib, change, status):
+    a = dict(hidden=64, num_q=4, gmap=[0, 1, 0, 1], ranks=[8, 8], value_rank=16, dtype=1, split=0,
+             head_dim=16)
+    a.update(change)
+    gm = (ctypes.c_int32 * 4)(*a["gmap"])
+    rk = (ctypes.c_int32 * 2)(*a["ranks"])
+    desc = capi.LayerDesc(a["hidden"], a["num_q"], 4, a["head_dim"], 2,
+                          ctypes.cast(gm, ctypes.POINTER(ctypes.c_int32)),
+                          ctypes.cast(rk, ctypes.POINTER(ctypes.c_int32)),
+                          a["value_rank"], a["dtype"], a["split"])
+    out = ctypes.c_void_p(12345)
+    st = lib.dckv_plan_create(ctypes.byref(desc), ctypes.byref(out))
+    assert capi.STATUS_NAMES[st] == status
+    assert out.value == 12345                       # untouched on failure
+    assert lib.dckv_last_error().decode().startswith("plan_create:")
+
+
+def test_workspace_bytes_grows_with_work():
+    wl = make_workload("gqa8b_b4_t32k")
+    p = _plan(wl)
+    a = p.workspace_bytes(4, 32768)
+    assert a > p.workspace_bytes(1, 32768) > 0
+    assert a >= p.workspace_bytes(4, 1024)
+    assert p.workspace_bytes(4, 0) > 0
+
+
+@pytest.mark.skipif(torch.cuda.is_available(), reason="raw fake pointers are only passed on a host without a GPU")
+def test_call_validation_never_launches(lib):
+    wl = make_workload("tiny_mha_f32")
+    p = _plan(wl)
+    h = p.handle
+    A = 1 << 20                                       # aligned fake address, never dereferenced
+    # append: null pointer, misalignment, bad sizes
+    assert lib.dckv_latent_append(h, None, 4, A, A, A, A, 4, None) == capi.DCKV_EINVAL
+    assert lib.dckv_latent_append(h, A + 2, 4, A, A, A, A, 4, None) == capi.DCKV_EALIGN
+    assert lib.dckv_latent_append(h, A, -1, A, A, A, A, 4, None) == capi.DCKV_EINVAL
+    assert lib.dckv_latent_append(h, A, 4, A, A, A, A, 0, None) == capi.DCKV_EINVAL
+    assert lib.dckv_latent_append(h, None, 0, None, None, None, None, 0, None) == capi.DCKV_OK
+    # decode
+    ws_need = p.workspace_bytes(1, 256)
+    args = [h, A, 1, A, 4, A, 4, A, 256, A, A, A, A, ws_need, None]
+
+    def call(**kw):
+        a = list(args)
+        idx = {"q": 1, "batch": 2, "pool": 3, "num_pages": 4, "table": 5, "max_pages": 6,
+               "lens": 7, "max_context": 8, "rk": 9, "rv": 10, "out": 11, "ws": 12, "ws_bytes": 13}
+        for k, v in kw.items():
+            a[idx[k]] = v
+        return lib.dckv_decode(*a)
+    assert call(q=None) == capi.DCKV_EINVAL
+    assert call(max_context=257) == capi.DCKV_EINVAL          # beyond max_pages * 64
+    assert call(max_context=-1) == capi.DCKV_EINVAL
+    assert call(num_pages=0) == capi.DCKV_EINVAL
+    assert call(max_pages=0) == capi.DCKV_EINVAL
+    assert call(batch=-2) == capi.DCKV_EINVAL
+    assert call(out=A + 4) == capi.DCKV_EALIGN
+    assert call(ws=A + 16) == capi.DCKV_EALIGN
+    assert call(ws_bytes=ws_need - 1) == capi.DCKV_EWORKSPACE
+    assert "workspace" in lib.dckv_last_error().decode()
+    assert call(batch=0) == capi.DCKV_OK                      # no-op
+
+
+def test_binding_rejects_host_tensors():
+    from paper_2607_24331_amd import decode, latent_append
+    wl = make_workload("tiny_mha_f32")
+    p = _plan(wl)
+    x = torch.zeros(4, 512)
+    with pytest.raises(ValueError, match="GPU"):
+        latent_append(p, x, torch.zeros(512, 128), torch.zeros(512, 128),
+                      torch.zeros(4, dtype=torch.int64), torch.zeros(4, p.page_elems))
+    with pytest.raises(ValueError, match="GPU"):
+        decode(p, torch.zeros(1, 8, 64), torch.zeros(4, p.page_elems), torch.zeros(1, 4, dtype=torch.int32),
+               torch.zeros(1, dtype=torch.int32), 256, torch.zeros(p.key_factor_elems),
+               torch.zeros(128, 512))
