@@ -35,6 +35,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mha_long_t128k")
     ap.add_argument("--split-tokens", type=int, default=0)
+    ap.add_argument("--head-slices", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle sample")
@@ -73,6 +74,15 @@ def device_inputs(wl, plan, torch):
         posn = torch.arange(p0, p0 + wl.append_tokens)
         d["slot"] = (table[0, posn // 64].long() * 64 + posn % 64).to(dev)
     return d
+
+
+def _auto_split(plan, wl, max_ctx):
+    """Split size the library picks when none is given (reported only)."""
+    if plan.geometry["mfma_path"]:
+        J = plan.geometry["head_slices"]
+        L = -(-wl.batch * max_ctx * J // 256)
+        return max(64, -(-L // 64) * 64)
+    return 1024
 
 
 def algorithmic_bytes(wl):
@@ -157,9 +167,11 @@ def main():
 
     wl = make_workload(args.workload)
     plan = Plan(wl.hidden, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_of_kv,
-                wl.group_rank, wl.value_rank, wl.dtype, args.split_tokens)
+                wl.group_rank, wl.value_rank, wl.dtype, args.split_tokens, args.head_slices)
+    mfma = bool(plan.geometry["mfma_path"])
     inp = device_inputs(wl, plan, torch)
     max_ctx = max(wl.seq_lens)
+    split_used = plan.split_tokens or _auto_split(plan, wl, max_ctx)
     out = torch.empty((wl.batch, wl.num_q_heads, wl.head_dim), dtype=torch.float32, device="cuda")
     ws = plan.new_workspace(wl.batch, max_ctx)
 
@@ -210,7 +222,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "bf16" if mfma else "f32",
         "data": "synthetic (seeded random latents, factors, queries and new tokens of the workload's shapes)",
         "config": {
             "workload": wl.name,
@@ -220,12 +232,13 @@ def main():
             "q_heads": wl.num_q_heads, "kv_heads": wl.num_kv_heads, "head_dim": wl.head_dim,
             "hidden": wl.hidden, "group_sizes": list(wl.group_sizes),
             "group_ranks": list(wl.group_rank), "value_rank": wl.value_rank,
-            "latent_dtype": wl.dtype, "split_tokens": plan.split_tokens,
+            "latent_dtype": wl.dtype, "split_tokens": split_used,
+            "head_slices": plan.geometry["head_slices"],
         },
         "context_tokens_per_s": sum(wl.seq_lens) / (ms_step * 1e-3),
         "step_hbm_gbs": (nb["decode_total"] + nb["append"]) / (ms_step * 1e-3) / 1e9,
         "roofline": {
-            "kernel": "split-K latent attention (split_valu)",
+            "kernel": "split-K latent attention (" + ("split_mfma" if mfma else "split_valu") + ")",
             "bound": "hbm",
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,

@@ -90,7 +90,11 @@ typedef struct dckv_layer_desc {
   int32_t value_rank;              /* r_v with 1 <= r_v <= min(m, H_kv*d_h) */
   int32_t latent_dtype;            /* dckv_dtype of latents, x and the L/R factors */
   int32_t split_tokens;            /* context tokens per decode work split; a
-                                      multiple of 64, or 0 for the default */
+                                      multiple of 64, or 0 to choose per call from
+                                      (batch, max_context) */
+  int32_t head_slices;             /* query-head slices served by separate decode
+                                      work-groups (bf16 path); 0 for the default
+                                      (one slice per 32 heads) */
 } dckv_layer_desc;
 
 /* Derived layout facts of a plan. */
@@ -100,7 +104,9 @@ typedef struct dckv_plan_geometry {
   int32_t value_rank;              /* r_v */
   int32_t q_per_kv;                /* H_q / H_kv */
   int32_t folded_query_len;        /* sum over query heads h of r_{g(h)} */
-  int32_t split_tokens;            /* effective tokens per decode split */
+  int32_t split_tokens;            /* tokens per decode split as described (0: per call) */
+  int32_t mfma_path;               /* 1 if decode uses the bf16 MFMA kernels */
+  int32_t head_slices;             /* query-head slices of the MFMA path (0 otherwise) */
   int64_t page_elems;              /* elements per page: 64*R_Kp + 64*r_v */
   int64_t value_base;              /* element offset of the value part in a page: 64*R_Kp */
   int64_t key_factor_elems;        /* elements of the concatenated R_g blocks */

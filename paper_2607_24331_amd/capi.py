@@ -41,6 +41,7 @@ class LayerDesc(ctypes.Structure):
         ("value_rank", ctypes.c_int32),
         ("latent_dtype", ctypes.c_int32),
         ("split_tokens", ctypes.c_int32),
+        ("head_slices", ctypes.c_int32),
     ]
 
 
@@ -52,6 +53,8 @@ class PlanGeometry(ctypes.Structure):
         ("q_per_kv", ctypes.c_int32),
         ("folded_query_len", ctypes.c_int32),
         ("split_tokens", ctypes.c_int32),
+        ("mfma_path", ctypes.c_int32),
+        ("head_slices", ctypes.c_int32),
         ("page_elems", ctypes.c_int64),
         ("value_base", ctypes.c_int64),
         ("key_factor_elems", ctypes.c_int64),

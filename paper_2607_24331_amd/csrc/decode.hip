@@ -6,6 +6,7 @@
 //          space (Sec. III-D shared value latent)
 //   merge  fixed ascending-split log-sum-exp merge, then o_h = (acc / l)
 //          R_v[:, kv(h) block] (one up-projection per head)
+#include <algorithm>
 #include <cmath>
 
 #include "device.h"
@@ -15,6 +16,8 @@ namespace dckv {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kTargetWorkgroups = 256;    // MI355X compute units
+constexpr int32_t kValuSplitTokens = 1024;
 constexpr int kAccPerThread = DCKV_MAX_VALUE_RANK / kThreads;
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -200,13 +203,38 @@ DecodeShape decode_shape(const dckv_plan& p, int32_t batch, int32_t max_context)
   DecodeShape s{};
   s.batch = batch;
   s.max_context = max_context;
-  s.split_tokens = p.split_tokens;
-  s.n_split = max_context > 0 ? (max_context + p.split_tokens - 1) / p.split_tokens : 1;
-  const size_t rows = size_t(batch) * p.Hq * s.n_split;
+  s.mfma = p.mfma_ok;
+  int64_t L = p.split_tokens;
+  if (L == 0) {
+    if (s.mfma) {
+      // about one work-group per compute unit over the whole batch
+      const int64_t tokens = int64_t(batch) * max_context * p.mfma.n_slices;
+      L = (tokens + kTargetWorkgroups - 1) / kTargetWorkgroups;
+      L = std::max<int64_t>(DCKV_PAGE_TOKENS, (L + DCKV_PAGE_TOKENS - 1) / DCKV_PAGE_TOKENS * DCKV_PAGE_TOKENS);
+    } else {
+      L = kValuSplitTokens;
+    }
+  }
+  if (s.mfma && L > mfma_max_split_tokens()) s.mfma = false;
+  s.split_tokens = int32_t(L);
+  s.n_split = max_context > 0 ? int32_t((max_context + L - 1) / L) : 1;
   s.off_qt = 0;
   s.off_ml = align_up(size_t(batch) * p.qlen * sizeof(float), 256);
-  s.off_acc = s.off_ml + align_up(rows * 2 * sizeof(float), 256);
-  s.bytes = s.off_acc + align_up(rows * p.rv * sizeof(float), 256);
+  if (s.mfma) {
+    const int64_t units = int64_t(batch) * s.n_split;
+    s.n_units = int32_t((units + 7) / 8 * 8);
+    s.n_rchunks = mfma_merge_rank_chunks(p);
+    const size_t nh = 16 * size_t(p.mfma.nt);
+    s.off_acc = s.off_ml;
+    const size_t part = size_t(batch) * p.mfma.n_slices * s.n_split * nh * (2 + size_t(p.rv));
+    s.off_opart = s.off_acc + align_up(part * sizeof(float), 256);
+    s.bytes = s.off_opart + align_up(size_t(batch) * p.Hq * p.rv * sizeof(float), 256);
+  } else {
+    const size_t rows = size_t(batch) * p.Hq * s.n_split;
+    s.off_acc = s.off_ml + align_up(rows * 2 * sizeof(float), 256);
+    s.off_opart = s.off_acc + align_up(rows * p.rv * sizeof(float), 256);
+    s.bytes = s.off_opart;
+  }
   return s;
 }
 
@@ -214,6 +242,16 @@ hipError_t launch_decode(const dckv_plan& p, const DecodeShape& shape, const flo
                          const void* pool, int64_t num_pages, const int32_t* page_table,
                          int32_t max_pages, const int32_t* seq_lens, const void* R_keys,
                          const void* R_value, float* out, void* workspace, hipStream_t stream) {
+  if (shape.mfma) {
+    float* qt = reinterpret_cast<float*>(static_cast<char*>(workspace) + shape.off_qt);
+    const float scale = kLog2e / std::sqrt(float(p.dh));
+    hipLaunchKernelGGL(fold_kernel<bf16>, dim3(p.Hq, shape.batch), dim3(kThreads), 0, stream, q,
+                       static_cast<const bf16*>(R_keys), qt, p.tables, scale);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_decode_mfma(p, shape, qt, pool, num_pages, page_table, max_pages, seq_lens,
+                              R_value, out, workspace, stream);
+  }
   if (p.dtype == DCKV_F32)
     return launch_decode_t<float>(p, shape, q, pool, num_pages, page_table, max_pages, seq_lens,
                                   R_keys, R_value, out, workspace, stream);

@@ -1,0 +1,573 @@
+// bf16 decode path on MFMA (gfx950).
+//
+// split_mfma: one 256-thread work-group (4 waves, one per SIMD) serves one
+// slice of query heads (all heads when H_q <= 32) over one context split, so
+// every latent byte of the split is read by exactly one work-group.  Per
+// 64-token page:
+//   scores   S^T[t][h] = sum_k Z_K[t][k] * Qblk[k][h], where Qblk is the
+//            block-diagonal matrix holding head h's folded query q~_h in its
+//            group's key columns (Sec. III-C: a head only meets its own group
+//            latent).  MFMA 16x16x32 bf16 with fp32 accumulation; q~ is split
+//            into bf16 hi + lo parts, so each score carries ~16 mantissa bits
+//            of q~ and exact bf16 latents.
+//   softmax  base-2 online softmax in fp32: per-head running max and sum,
+//            tile maxima exchanged through LDS (two barriers a page).
+//   values   acc^T[j][h] += sum_t Z_v^T[j][t] * p^T[t][h] on MFMA, p rounded
+//            to bf16, accumulated in value-latent space (Sec. III-D: one value
+//            latent shared by every head).
+// Each wave streams its own operands with 16-byte loads straight into a
+// 16-deep register ring, so 16 KB per wave stay in flight.
+//
+// merge_mfma: fixed ascending-split log-sum-exp merge of the partials into
+// the normalised value-latent output a_h (fp32).
+// upproj: o_h = a_h R_v[:, kv(h) block] (Sec. III-A z R, Sec. III-D R_v).
+#include <cmath>
+
+#include "device.h"
+#include "internal.h"
+
+namespace dckv {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kRing = 16;                 // loads in flight per wave
+constexpr int kPageSlots = 256;           // pages per split the LDS page list holds
+constexpr int kPStride = 72;              // bf16 per head row of the p tile (64 + pad)
+constexpr int kMergeRanks = 16;           // value ranks per merge work-group
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Word 3 of a raw buffer descriptor on gfx9-family parts (32-bit data
+// format, no swizzle); loads at or past num_records return zero.
+constexpr int kRsrcWord3 = 0x00020000;
+constexpr int kOutOfRange = 0x40000000;   // byte offset beyond any page
+
+// One producer block: RING consecutive items of one page, all keys or all
+// values (kind 2: past the split, every load reads zero).
+struct ProdBlock {
+  __amdgpu_buffer_rsrc_t rsrc;
+  int kind;
+  int base;    // byte offset of the block's first item, lane part excluded
+  int idx0;    // index of the block's first item in the page's stream
+  int nval;    // valid tokens of the page
+};
+
+__device__ __forceinline__ floatx4 mfma(u32x4 a, u32x4 b, floatx4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ u32x4 load16(const bf16* p) {
+  return *reinterpret_cast<const u32x4*>(p);
+}
+
+// Keep the first `n` (0..8) bf16 of a 16-byte vector, zero the rest.
+__device__ __forceinline__ u32x4 keep_first(u32x4 v, int n) {
+  u32x4 r;
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    const uint32_t lo = (2 * d < n) ? 0x0000FFFFu : 0u;
+    const uint32_t hi = (2 * d + 1 < n) ? 0xFFFF0000u : 0u;
+    r[d] = v[d] & (lo | hi);
+  }
+  return r;
+}
+
+__device__ __forceinline__ float wave_max16(float v) {   // over lanes l, l^16, l^32, l^48
+  v = fmaxf(v, __shfl_xor(v, 16));
+  v = fmaxf(v, __shfl_xor(v, 32));
+  return v;
+}
+__device__ __forceinline__ float wave_sum16(float v) {
+  v += __shfl_xor(v, 16);
+  v += __shfl_xor(v, 32);
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// W waves (4 or 8) a work-group; NT 16-head tiles; at most MTW value M-tiles
+// (16 ranks) a wave; RING loads in flight a wave.
+template <int W, int NT, int MTW, int RING>
+__global__ __launch_bounds__(W * 64, 1) void split_mfma(
+    const float* __restrict__ qt, const bf16* __restrict__ pool, int64_t num_pages,
+    const int32_t* __restrict__ page_table, int max_pages, const int32_t* __restrict__ seq_lens,
+    int max_context, int split_tokens, int n_split, int n_units, int RK, int RKp, int rv,
+    int64_t page_elems, int64_t value_base, float* __restrict__ part, HeadTables tb, MfmaTables mt) {
+  constexpr int NH = 16 * NT;                          // head slots of the slice
+  constexpr int SW = (4 * NT < W) ? 4 * NT : W;        // waves holding score tiles
+  constexpr int MPW = (4 * NT) / SW;                   // score M-tiles (16 tokens) a scoring wave
+  constexpr int NV = ((2 * MTW + RING - 1) / RING) * RING;   // value items a page (padded)
+  static_assert(RING % 2 == 0 && RING % MPW == 0, "ring blocks hold whole chunks and k-steps");
+  extern __shared__ __align__(16) unsigned char smem[];
+
+  const int J = mt.n_slices;
+  const int Lid = blockIdx.x;
+  const int grp = Lid / (8 * J), rr = Lid % (8 * J);
+  const int slice = rr / 8;
+  const int u = grp * 8 + (rr % 8);       // all slices of unit u share an XCD (ids equal mod 8)
+  if (u >= n_units) return;               // n_units = batch * n_split (the grid is padded)
+  const int b = u / n_split, split = u % n_split;
+  int T_b = seq_lens[b];
+  T_b = T_b < 0 ? 0 : (T_b > max_context ? max_context : T_b);
+  const int t0 = split * split_tokens;
+  const int t1 = min(t0 + split_tokens, T_b);
+  if (t0 >= t1) return;                   // the merge only reads splits holding tokens
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, provably uniform
+  const int lr = lane & 15, lq = lane >> 4;
+  const int np = (t1 - t0 + 63) / 64;
+
+  // ---- LDS carve-up
+  const int nch0 = mt.kc1[slice][0] - mt.kc0[slice][0];
+  const int npairs = nch0 + (NT > 1 ? mt.kc1[slice][1] - mt.kc0[slice][1] : 0);
+  u32x4* qblk = reinterpret_cast<u32x4*>(smem);                         // [npairs][2][64]
+  bf16* p_lds = reinterpret_cast<bf16*>(smem + size_t(npairs) * 2048);  // [32][kPStride]
+  float* red_max = reinterpret_cast<float*>(p_lds + 32 * kPStride);     // [8][32]
+  float* red_sum = red_max + 8 * 32;                                    // [8][32]
+  int* pids = reinterpret_cast<int*>(red_sum + 8 * 32);                 // [kPageSlots]
+
+  for (int i = tid; i < np; i += W * 64) {
+    const int pg = page_table[int64_t(b) * max_pages + (t0 >> 6) + i];
+    pids[i] = (pg >= 0 && pg < num_pages) ? pg : -1;
+  }
+
+  // ---- wave roles
+  const bool scoring = w < SW;
+  const int n_w = scoring ? (w * MPW) / 4 : 0;        // score N-tile
+  const int mb_w = scoring ? (w * MPW) % 4 : 0;       // first score M-tile
+  const int kc0_w = mt.kc0[slice][n_w];
+  const int nch_w = mt.kc1[slice][n_w] - kc0_w;
+  const int nk_real = scoring ? nch_w * MPW : 0;      // key items a page
+  const int NK = (nk_real + RING - 1) / RING * RING;  // padded to whole ring blocks
+  const int pair0_w = (n_w == 0) ? 0 : nch0;
+  const int mt0_w = w * mt.mtw;
+  const int mcnt_w = max(0, min(mt.mtw, mt.mt_v - mt0_w));
+  const int kc_last = mt.kc1[slice][n_w] - 1;
+  const int kvalid_last = min(8, max(0, RK - (32 * kc_last + 8 * lq)));
+
+  // ---- producer.  The item stream of a page is NK key items (chunk-major,
+  // M-tile minor) then NV value items (M-tile-major, k-step minor).  The
+  // producer runs exactly one ring block ahead of the consumer and both
+  // lengths are whole blocks, so a producer block never spans two pages or
+  // two kinds: its page and kind are set once per block, and each issue is a
+  // single unconditional 16-byte buffer load (out-of-range offsets read 0).
+  const int lane_key = 2 * (lr * RKp + 8 * lq);       // byte offsets of this lane
+  const int lane_val = 2 * (lr * 64 + 8 * lq);
+  const int page_bytes = int(page_elems * 2);
+  const int blocks_pp = (NK + NV) / RING;             // producer blocks a page
+  int prod_block = 0;                                 // producer block counter over the split
+  __syncthreads();                                    // pids ready
+  auto setup = [&](int pblk) {
+    ProdBlock r;
+    const int page = pblk / blocks_pp;
+    const int blk = pblk - page * blocks_pp;
+    int pid = -1;
+    if (page < np) pid = __builtin_amdgcn_readfirstlane(pids[page]);
+    const bf16* base = pid >= 0 ? pool + int64_t(pid) * page_elems : pool;
+    r.rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(base), 0,
+                                               pid >= 0 ? page_bytes : 0, kRsrcWord3);
+    r.nval = page < np ? min(64, (t1 - t0) - page * 64) : 0;
+    r.idx0 = blk * RING;                              // first item of the block
+    r.kind = page >= np ? 2 : (r.idx0 < NK ? 0 : 1);
+    r.base = r.kind == 0 ? 2 * (16 * mb_w * RKp + 32 * (kc0_w + r.idx0 / MPW))
+                         : 2 * (int(value_base) + 16 * (mt0_w + (r.idx0 - NK) / 2) * 64);
+    return r;
+  };
+  // issue item s (compile-time slot) of producer block pb
+  auto issue = [&](const ProdBlock& pb, int s) -> u32x4 {
+    int off = kOutOfRange;
+    if (pb.kind == 0) {
+      const int i = pb.idx0 + s;
+      const int c = kc0_w + i / MPW;
+      const int o = pb.base + 2 * (16 * (s % MPW) * RKp + 32 * (s / MPW)) + lane_key;
+      const bool ok = (i < nk_real) & (32 * c + 8 * lq < RK);     // no short-circuit branches
+      off = ok ? o : kOutOfRange;
+    } else if (pb.kind == 1) {
+      const int mtl = (pb.idx0 - NK + s) >> 1;
+      const int o = pb.base + 2 * (16 * (s >> 1) * 64 + 32 * (s & 1)) + lane_val;
+      const bool ok = (mtl < mcnt_w) & (16 * (mt0_w + mtl) + lr < rv) & (32 * (s & 1) + 8 * lq < pb.nval);
+      off = ok ? o : kOutOfRange;
+    }
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(pb.rsrc, off, 0, 0));
+  };
+
+  u32x4 ring[RING];
+  {
+    const ProdBlock pb0 = setup(prod_block++);
+#pragma unroll
+    for (int s = 0; s < RING; ++s) ring[s] = issue(pb0, s);
+  }
+
+  // ---- block-diagonal folded query, hi/lo bf16, in MFMA B-operand order:
+  // block (tile n, chunk c), lane l, element e  <->  key column 32c + 8(l/16) + e,
+  // head slot 16n + l%16.
+  {
+    const float* qb = qt + int64_t(b) * tb.qlen;
+    for (int idx = tid; idx < npairs * 64; idx += W * 64) {
+      const int pr = idx >> 6, l = idx & 63;
+      const int n = (NT > 1 && pr >= nch0) ? 1 : 0;
+      const int c = mt.kc0[slice][n] + pr - (n ? nch0 : 0);
+      const int h = mt.hord[slice][16 * n + (l & 15)];
+      int lo = 0, cnt = 0, qo = 0;
+      if (h >= 0) {
+        lo = tb.koff_of_q[h];
+        cnt = tb.rank_of_q[h];
+        qo = tb.qoff[h];
+      }
+      uint32_t hi_w[4], lo_w[4];
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2) {
+        uint32_t hw = 0, lw = 0;
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const int k = 32 * c + 8 * (l >> 4) + 2 * e2 + half;
+          float v = 0.f;
+          if (k >= lo && k < lo + cnt) v = qb[qo + k - lo];
+          const bf16 vh = static_cast<bf16>(v);
+          const bf16 vl = static_cast<bf16>(v - static_cast<float>(vh));
+          hw |= uint32_t(__builtin_bit_cast(uint16_t, vh)) << (16 * half);
+          lw |= uint32_t(__builtin_bit_cast(uint16_t, vl)) << (16 * half);
+        }
+        hi_w[e2] = hw;
+        lo_w[e2] = lw;
+      }
+      qblk[(pr * 2 + 0) * 64 + l] = u32x4{hi_w[0], hi_w[1], hi_w[2], hi_w[3]};
+      qblk[(pr * 2 + 1) * 64 + l] = u32x4{lo_w[0], lo_w[1], lo_w[2], lo_w[3]};
+    }
+  }
+  __syncthreads();
+
+  floatx4 acc[MTW][NT];
+#pragma unroll
+  for (int i = 0; i < MTW; ++i)
+#pragma unroll
+    for (int n = 0; n < NT; ++n) acc[i][n] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float m_run[NT], l_run[NT];
+#pragma unroll
+  for (int n = 0; n < NT; ++n) {
+    m_run[n] = -INFINITY;
+    l_run[n] = 0.f;
+  }
+  const int pmax_pair = pair0_w + max(nch_w, 1) - 1;    // clamp for padded key items
+
+  for (int page = 0; page < np; ++page) {
+    const int nval = min(64, (t1 - t0) - page * 64);
+    const bool pvalid = pids[page] >= 0;
+
+    // ---- scores: MPW M-tiles (16 tokens each) of this wave's N-tile
+    floatx4 S[MPW];
+#pragma unroll
+    for (int m = 0; m < MPW; ++m) S[m] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int kb = 0; kb < NK; kb += RING) {
+      const ProdBlock pbk = setup(prod_block++);
+      u32x4 bhi = {0u, 0u, 0u, 0u}, blo = {0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int s = 0; s < RING; ++s) {
+        const int c = (kb + s) / MPW;     // chunk offset inside the tile's range
+        if (s % MPW == 0) {
+          const int pr = min(pair0_w + c, pmax_pair);
+          bhi = qblk[(pr * 2 + 0) * 64 + lane];
+          blo = qblk[(pr * 2 + 1) * 64 + lane];
+        }
+        u32x4 a = ring[s];
+        if (kc0_w + c == kc_last) a = keep_first(a, kvalid_last);
+        S[s % MPW] = mfma(a, bhi, S[s % MPW]);
+        S[s % MPW] = mfma(a, blo, S[s % MPW]);
+        ring[s] = issue(pbk, s);
+      }
+    }
+
+    // ---- softmax, part 1: tile maxima
+    if (scoring) {
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int m = 0; m < MPW; ++m)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int tok = 16 * (mb_w + m) + 4 * lq + v;
+          if (!pvalid || tok >= nval) S[m][v] = -INFINITY;
+          tmax = fmaxf(tmax, S[m][v]);
+        }
+      tmax = wave_max16(tmax);
+      if (lane < 16) red_max[w * 32 + lane] = tmax;
+    }
+    __syncthreads();
+
+    // ---- part 2: new maxima, p for own tokens, partial row sums
+    float m_new[NT], alpha[NT];
+#pragma unroll
+    for (int n = 0; n < NT; ++n) {
+      float mx = m_run[n];
+#pragma unroll
+      for (int ww = 0; ww < SW; ++ww)
+        if ((ww * MPW) / 4 == n) mx = fmaxf(mx, red_max[ww * 32 + lr]);
+      m_new[n] = mx;
+      alpha[n] = (mx == -INFINITY) ? 1.f : exp2f(m_run[n] - mx);
+    }
+    if (scoring) {
+      float psum = 0.f;
+      const float mw = (NT > 1 && n_w == 1) ? m_new[NT - 1] : m_new[0];   // no dynamic register index
+#pragma unroll
+      for (int m = 0; m < MPW; ++m) {
+        uint32_t pk[2];
+#pragma unroll
+        for (int v2 = 0; v2 < 2; ++v2) {
+          uint32_t word = 0;
+#pragma unroll
+          for (int half = 0; half < 2; ++half) {
+            const float sc = S[m][2 * v2 + half];
+            const float pv = (sc == -INFINITY) ? 0.f : exp2f(sc - mw);
+            const bf16 pb = static_cast<bf16>(pv);
+            psum += static_cast<float>(pb);
+            word |= uint32_t(__builtin_bit_cast(uint16_t, pb)) << (16 * half);
+          }
+          pk[v2] = word;
+        }
+        const int tok = 16 * (mb_w + m) + 4 * lq;
+        *reinterpret_cast<uint2*>(p_lds + (16 * n_w + lr) * kPStride + tok) = uint2{pk[0], pk[1]};
+      }
+      psum = wave_sum16(psum);
+      if (lane < 16) red_sum[w * 32 + lane] = psum;
+    }
+    __syncthreads();
+
+    // ---- part 3: running sums, rescale, p operands
+    bool rescale = false;
+#pragma unroll
+    for (int n = 0; n < NT; ++n) {
+      float sum = 0.f;
+#pragma unroll
+      for (int ww = 0; ww < SW; ++ww)
+        if ((ww * MPW) / 4 == n) sum += red_sum[ww * 32 + lr];
+      l_run[n] = l_run[n] * alpha[n] + sum;
+      m_run[n] = m_new[n];
+      rescale = rescale || alpha[n] != 1.f;
+    }
+    u32x4 pB[NT][2];
+#pragma unroll
+    for (int n = 0; n < NT; ++n)
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+        pB[n][ks] = *reinterpret_cast<const u32x4*>(p_lds + (16 * n + lr) * kPStride + 32 * ks + 8 * lq);
+    if (__any(rescale)) {                 // the running maximum moved for some head
+#pragma unroll
+      for (int i = 0; i < MTW; ++i)
+#pragma unroll
+        for (int n = 0; n < NT; ++n) acc[i][n] *= alpha[n];
+    }
+    // token masks of the two k-steps on a partial page
+    const int keep0 = min(8, max(0, nval - 8 * lq));
+    const int keep1 = min(8, max(0, nval - 32 - 8 * lq));
+
+    // ---- values: acc^T[rank][head] += Z_v^T[rank][tok] p^T[tok][head]
+#pragma unroll
+    for (int vb = 0; vb < NV; vb += RING) {
+      const ProdBlock pbv = setup(prod_block++);
+#pragma unroll
+      for (int s = 0; s < RING; ++s) {
+        const int i = vb + s;
+        const int mtl = i >> 1, ks = i & 1;
+        u32x4 a = ring[s];
+        if (nval < 64) a = keep_first(a, ks ? keep1 : keep0);
+        if (mtl < MTW) {
+#pragma unroll
+          for (int n = 0; n < NT; ++n) acc[mtl][n] = mfma(a, pB[n][ks], acc[mtl][n]);
+        }
+        ring[s] = issue(pbv, s);
+      }
+    }
+  }
+
+  // ---- partials: m[NH], l[NH], acc[rank][NH] (head slot fastest)
+  float* pb = part + ((int64_t(b) * J + slice) * n_split + split) * int64_t(NH * (2 + rv));
+  if (w == 0 && lane < 16) {
+#pragma unroll
+    for (int n = 0; n < NT; ++n) {
+      pb[16 * n + lane] = m_run[n];
+      pb[NH + 16 * n + lane] = l_run[n];
+    }
+  }
+  float* pa = pb + 2 * NH;
+#pragma unroll
+  for (int i = 0; i < MTW; ++i) {
+    if (i < mcnt_w) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int rank = 16 * (mt0_w + i) + 4 * lq + v;
+        if (rank < rv) {
+#pragma unroll
+          for (int n = 0; n < NT; ++n) pa[int64_t(rank) * NH + 16 * n + lr] = acc[i][n][v];
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Merge: a[b][h][r] = sum_s 2^(m_s - M) acc_s[r] / sum_s 2^(m_s - M) l_s,
+// splits in ascending order.  Grid (rank chunks, batch * slices).
+__global__ __launch_bounds__(256) void merge_mfma(const float* __restrict__ part,
+                                                  const int32_t* __restrict__ seq_lens,
+                                                  int max_context, int split_tokens, int n_split,
+                                                  int rv, int nh, float* __restrict__ amerged,
+                                                  HeadTables tb, MfmaTables mt) {
+  const int rc = blockIdx.x;
+  const int bj = blockIdx.y;
+  const int J = mt.n_slices;
+  const int b = bj / J, slice = bj % J;
+  const int tid = threadIdx.x;
+  __shared__ float sM[32], sInvL[32];
+  int T_b = seq_lens[b];
+  T_b = T_b < 0 ? 0 : (T_b > max_context ? max_context : T_b);
+  const int ns = (T_b + split_tokens - 1) / split_tokens;
+  const int64_t stride = int64_t(nh) * (2 + rv);
+  const float* pb = part + (int64_t(b) * J + slice) * n_split * stride;
+  if (tid < nh) {
+    float M = -INFINITY;
+    for (int s = 0; s < ns; ++s) M = fmaxf(M, pb[s * stride + tid]);
+    float L = 0.f;
+    if (M != -INFINITY)
+      for (int s = 0; s < ns; ++s) L += exp2f(pb[s * stride + tid] - M) * pb[s * stride + nh + tid];
+    sM[tid] = M;
+    sInvL[tid] = (L > 0.f) ? 1.f / L : 0.f;
+  }
+  __syncthreads();
+  const int r0 = rc * kMergeRanks;
+  for (int e = tid; e < kMergeRanks * nh; e += 256) {
+    const int hp = e % nh, r = r0 + e / nh;
+    const int h = mt.hord[slice][hp];
+    if (r >= rv || h < 0) continue;
+    const float M = sM[hp];
+    float a = 0.f;
+    if (M != -INFINITY) {
+      const float* src = pb + 2 * nh + int64_t(r) * nh + hp;
+      int s = 0;
+      for (; s + 4 <= ns; s += 4) {
+        const float m0 = pb[(s + 0) * stride + hp], m1 = pb[(s + 1) * stride + hp];
+        const float m2 = pb[(s + 2) * stride + hp], m3 = pb[(s + 3) * stride + hp];
+        const float a0 = src[(s + 0) * stride], a1 = src[(s + 1) * stride];
+        const float a2 = src[(s + 2) * stride], a3 = src[(s + 3) * stride];
+        a = fmaf(exp2f(m0 - M), a0, a);
+        a = fmaf(exp2f(m1 - M), a1, a);
+        a = fmaf(exp2f(m2 - M), a2, a);
+        a = fmaf(exp2f(m3 - M), a3, a);
+      }
+      for (; s < ns; ++s) a = fmaf(exp2f(pb[s * stride + hp] - M), src[s * stride], a);
+      a *= sInvL[hp];
+    }
+    amerged[(int64_t(b) * tb.n_q_heads + h) * rv + r] = a;
+  }
+}
+
+// Up-projection o[b][h][d] = sum_r a[b][h][r] R_v[r][kv(h)*d_h + d].
+// Grid (query heads, batch); 256 threads = d columns x rank quarters.
+__global__ __launch_bounds__(256) void upproj(const float* __restrict__ amerged,
+                                              const bf16* __restrict__ Rv,
+                                              float* __restrict__ out, int rv, HeadTables tb) {
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int dh = tb.head_dim, n = tb.n_kv_heads * dh;
+  const int kv = h / tb.q_per_kv;
+  __shared__ float sa[DCKV_MAX_VALUE_RANK];
+  __shared__ float red[256];
+  const float* a = amerged + (int64_t(b) * tb.n_q_heads + h) * rv;
+  for (int r = tid; r < rv; r += 256) sa[r] = a[r];
+  __syncthreads();
+  // thread -> (column d, rank group); 2 columns a thread when d_h > 128
+  const int groups = 256 / min(256, dh);
+  for (int d0 = 0; d0 < dh; d0 += 256 / groups) {
+    const int d = d0 + tid % (256 / groups), g = tid / (256 / groups);
+    float acc = 0.f;
+    if (d < dh) {
+      const bf16* col = Rv + int64_t(kv) * dh + d;
+      for (int r = g; r < rv; r += groups) acc = fmaf(sa[r], static_cast<float>(col[int64_t(r) * n]), acc);
+    }
+    red[tid] = acc;
+    __syncthreads();
+    if (g == 0 && d < dh) {
+      float o = 0.f;
+      for (int k = 0; k < groups; ++k) o += red[k * (256 / groups) + tid % (256 / groups)];
+      out[(int64_t(b) * tb.n_q_heads + h) * dh + d] = o;
+    }
+    __syncthreads();
+  }
+}
+
+template <int W, int NT, int MTW>
+hipError_t launch_split(const dckv_plan& p, const DecodeShape& sh, const float* qt,
+                        const void* pool, int64_t num_pages, const int32_t* page_table,
+                        int32_t max_pages, const int32_t* seq_lens, float* part,
+                        size_t lds, hipStream_t stream) {
+  constexpr int RING = (W == 4) ? 16 : 8;
+  auto kern = split_mfma<W, NT, MTW, RING>;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+  if (e != hipSuccess) return e;
+  const int grid = sh.n_units * p.mfma.n_slices;
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(W * 64), lds, stream, qt,
+                     static_cast<const bf16*>(pool), num_pages, page_table, max_pages, seq_lens,
+                     sh.max_context, sh.split_tokens, sh.n_split, sh.batch * sh.n_split, p.RK, p.RKp, p.rv,
+                     p.page_elems, p.value_base, part, p.tables, p.mfma);
+  return hipGetLastError();
+}
+
+template <int W, int NT>
+hipError_t launch_split_w(const dckv_plan& p, const DecodeShape& sh, const float* qt,
+                          const void* pool, int64_t num_pages, const int32_t* page_table,
+                          int32_t max_pages, const int32_t* seq_lens, float* part, size_t lds,
+                          hipStream_t stream) {
+  const int mtw = p.mfma.mtw;
+  if (mtw <= 8)
+    return launch_split<W, NT, 8>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part, lds, stream);
+  if (mtw <= 16)
+    return launch_split<W, NT, 16>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part, lds, stream);
+  if (NT == 1 && mtw <= 32)
+    return launch_split<W, NT, (NT == 1 ? 32 : 16)>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part, lds, stream);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+size_t mfma_split_lds_bytes(const dckv_plan& p) {
+  return size_t(p.mfma.max_pairs) * 2048 + 32 * kPStride * 2 + 2 * 8 * 32 * 4 + kPageSlots * 4;
+}
+
+int mfma_merge_rank_chunks(const dckv_plan& p) { return (p.rv + kMergeRanks - 1) / kMergeRanks; }
+
+int mfma_max_split_tokens() { return kPageSlots * DCKV_PAGE_TOKENS; }
+
+hipError_t launch_decode_mfma(const dckv_plan& p, const DecodeShape& sh, const float* qt,
+                              const void* pool, int64_t num_pages, const int32_t* page_table,
+                              int32_t max_pages, const int32_t* seq_lens, const void* R_value,
+                              float* out, void* workspace, hipStream_t stream) {
+  char* ws = static_cast<char*>(workspace);
+  float* part = reinterpret_cast<float*>(ws + sh.off_acc);
+  float* amerged = reinterpret_cast<float*>(ws + sh.off_opart);
+  const size_t lds = mfma_split_lds_bytes(p);
+  hipError_t e;
+  if (p.prof_before && (e = hipEventRecord(p.prof_before, stream)) != hipSuccess) return e;
+  if (p.mfma.waves == 4)
+    e = p.mfma.nt == 1
+            ? launch_split_w<4, 1>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part, lds, stream)
+            : launch_split_w<4, 2>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part, lds, stream);
+  else
+    e = p.mfma.nt == 1
+            ? launch_split_w<8, 1>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part, lds, stream)
+            : launch_split_w<8, 2>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part, lds, stream);
+  if (e != hipSuccess) return e;
+  if (p.prof_after && (e = hipEventRecord(p.prof_after, stream)) != hipSuccess) return e;
+  const int nh = 16 * p.mfma.nt;
+  hipLaunchKernelGGL(merge_mfma, dim3(sh.n_rchunks, sh.batch * p.mfma.n_slices), dim3(256), 0,
+                     stream, part, seq_lens, sh.max_context, sh.split_tokens, sh.n_split, p.rv, nh,
+                     amerged, p.tables, p.mfma);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(upproj, dim3(p.Hq, sh.batch), dim3(256), 0, stream, amerged,
+                     static_cast<const bf16*>(R_value), out, p.rv, p.tables);
+  return hipGetLastError();
+}
+
+}  // namespace dckv

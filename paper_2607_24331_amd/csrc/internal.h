@@ -27,32 +27,71 @@ struct HeadTables {
   int64_t roff_of_q[DCKV_MAX_HEADS];         // element offset of R_g
 };
 
+constexpr int kMaxSlices = 4;     // head slices of the MFMA decode path
+constexpr int kSliceHeads = 32;   // at most two 16-head MFMA tiles per slice
+
+// Schedule of the MFMA decode path (bf16 latents), fixed by the plan.  Query
+// heads are ordered by (group, head) and cut into J slices of at most 32;
+// a work-group serves one slice of one context split, so each group's key
+// columns form one contiguous range and, with J = 1, every latent byte is
+// read by exactly one work-group.
+struct MfmaTables {
+  int32_t n_slices;                        // J
+  int32_t nt;                              // 16-head MFMA tiles per slice (1 or 2)
+  int32_t mt_v;                            // value M-tiles: ceil(r_v / 16)
+  int32_t waves;                           // waves a work-group: 4 or 8
+  int32_t mtw;                             // value M-tiles per wave: ceil(mt_v / waves)
+  int32_t max_pairs;                       // most LDS query blocks of any slice
+  int32_t slice_heads[kMaxSlices];         // real heads in slice s
+  int32_t hord[kMaxSlices][kSliceHeads];   // head slot -> query head, -1 for padding
+  int32_t kc0[kMaxSlices][2];              // first 32-column key chunk of (slice, tile)
+  int32_t kc1[kMaxSlices][2];              // one past the last
+};
+
 // Launch shape of one decode call, fixed by the plan and (batch, max_context).
 struct DecodeShape {
   int32_t batch;
   int32_t max_context;
   int32_t split_tokens;
   int32_t n_split;          // ceil(max_context / split_tokens), at least 1
+  bool mfma;                // bf16 MFMA path (else the portable VALU path)
+  int32_t n_units;          // batch * n_split rounded up to a multiple of 8: grid units (MFMA path)
+  int32_t n_rchunks;        // value-rank chunks of the merge (MFMA path)
   size_t off_qt;            // workspace byte offsets
   size_t off_ml;
   size_t off_acc;
+  size_t off_opart;
   size_t bytes;
 };
 
 }  // namespace dckv
 
 struct dckv_plan {
-  int32_t m, Hq, Hkv, dh, G, rv, dtype, split_tokens;
+  int32_t m, Hq, Hkv, dh, G, rv, dtype, split_tokens, head_slices;
   int32_t RK, RKp, qpk, qlen;
   int64_t page_elems, value_base, key_factor_elems;
   std::vector<int32_t> group_of_kv, ranks, hg, pos_in_group, koff, qoff;
   std::vector<int64_t> roff;
   dckv::HeadTables tables;
+  bool mfma_ok = false;              // bf16 MFMA decode path applies
+  dckv::MfmaTables mfma{};
   hipEvent_t prof_before = nullptr;  // benchmark instrumentation of the split kernel
   hipEvent_t prof_after = nullptr;
 };
 
 namespace dckv {
+
+// Builds plan.mfma and sets plan.mfma_ok (host only, no HIP call).
+void build_mfma_tables(dckv_plan& p);
+
+// MFMA decode path (decode_mfma.hip).
+size_t mfma_split_lds_bytes(const dckv_plan& p);
+int mfma_merge_rank_chunks(const dckv_plan& p);
+int mfma_max_split_tokens();
+hipError_t launch_decode_mfma(const dckv_plan& p, const DecodeShape& sh, const float* qt,
+                              const void* pool, int64_t num_pages, const int32_t* page_table,
+                              int32_t max_pages, const int32_t* seq_lens, const void* R_value,
+                              float* out, void* workspace, hipStream_t stream);
 
 // Defined in the kernel sources.
 DecodeShape decode_shape(const dckv_plan& p, int32_t batch, int32_t max_context);

@@ -27,9 +27,66 @@ int fail(int status, const char* fmt, ...) {
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
-constexpr int32_t kDefaultSplitTokens = 1024;
-
 }  // namespace
+
+namespace dckv {
+
+void build_mfma_tables(dckv_plan& p) {
+  p.mfma_ok = false;
+  p.mfma = MfmaTables{};
+  if (p.dtype != DCKV_BF16) return;
+  MfmaTables& t = p.mfma;
+  // Query heads ordered by (group of their KV head, head index): the heads
+  // of one group are adjacent, so a tile's key columns are one range.
+  std::vector<int32_t> order(p.Hq);
+  for (int32_t h = 0; h < p.Hq; ++h) order[h] = h;
+  std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
+    return p.group_of_kv[a / p.qpk] < p.group_of_kv[b / p.qpk];
+  });
+  int32_t J = p.head_slices > 0 ? p.head_slices : (p.Hq + kSliceHeads - 1) / kSliceHeads;
+  if (J > kMaxSlices || J > p.Hq) return;
+  const int32_t per = (p.Hq + J - 1) / J;
+  if (per > kSliceHeads) return;
+  t.n_slices = J;
+  t.nt = (per + 15) / 16;
+  int32_t max_pairs = 0;
+  for (int32_t s = 0; s < J; ++s) {
+    const int32_t h0 = std::min(p.Hq, s * per), h1 = std::min(p.Hq, (s + 1) * per);
+    t.slice_heads[s] = h1 - h0;
+    for (int32_t i = 0; i < kSliceHeads; ++i) t.hord[s][i] = (h0 + i < h1) ? order[h0 + i] : -1;
+    int32_t pairs = 0;
+    for (int32_t n = 0; n < t.nt; ++n) {
+      int32_t lo = p.RK, hi = 0;
+      for (int32_t i = 16 * n; i < 16 * n + 16; ++i) {
+        const int32_t h = t.hord[s][i];
+        if (h < 0) continue;
+        const int32_t g = p.group_of_kv[h / p.qpk];
+        lo = std::min(lo, p.koff[g]);
+        hi = std::max(hi, p.koff[g] + p.ranks[g]);
+      }
+      if (hi <= lo) {
+        t.kc0[s][n] = t.kc1[s][n] = 0;
+        continue;
+      }
+      t.kc0[s][n] = lo / 32;
+      t.kc1[s][n] = (hi + 31) / 32;
+      pairs += t.kc1[s][n] - t.kc0[s][n];
+    }
+    max_pairs = std::max(max_pairs, pairs);
+  }
+  t.max_pairs = max_pairs;
+  t.mt_v = (p.rv + 15) / 16;
+  // Accumulators take nt * mtw * 4 registers a lane: four waves while that
+  // stays within 128, else eight waves (two a SIMD) with half the ranks each.
+  t.waves = (t.nt * ((t.mt_v + 3) / 4) <= 32) ? 4 : 8;
+  t.mtw = (t.mt_v + t.waves - 1) / t.waves;
+  if (t.nt * t.mtw > 32) return;               // beyond 128 accumulator registers a lane
+  const int64_t lds = int64_t(max_pairs) * 2048 + 32 * 72 * 2 + 2 * 8 * 32 * 4 + 256 * 4;
+  if (lds > 160 * 1024) return;
+  p.mfma_ok = true;
+}
+
+}  // namespace dckv
 
 extern "C" {
 
@@ -58,6 +115,9 @@ int dckv_plan_create(const dckv_layer_desc* d, dckv_plan** out) {
   if (d->split_tokens < 0 || d->split_tokens % DCKV_PAGE_TOKENS != 0 || d->split_tokens > (1 << 24))
     return fail(DCKV_EINVAL, "plan_create: split_tokens %d is not 0 or a positive multiple of %d",
                 d->split_tokens, DCKV_PAGE_TOKENS);
+  if (d->head_slices < 0 || d->head_slices > DCKV_MAX_HEADS)
+    return fail(DCKV_EINVAL, "plan_create: head_slices %d outside [0,%d]", d->head_slices,
+                DCKV_MAX_HEADS);
 
   const int32_t Hkv = d->num_kv_heads, G = d->num_groups, dh = d->head_dim;
   std::vector<int32_t> hg(G, 0), pos(Hkv, 0);
@@ -90,7 +150,8 @@ int dckv_plan_create(const dckv_layer_desc* d, dckv_plan** out) {
     p->G = G;
     p->rv = d->value_rank;
     p->dtype = d->latent_dtype;
-    p->split_tokens = d->split_tokens ? d->split_tokens : kDefaultSplitTokens;
+    p->split_tokens = d->split_tokens;
+    p->head_slices = d->head_slices;
     p->group_of_kv.assign(d->group_of_kv_head, d->group_of_kv_head + Hkv);
     p->ranks.assign(d->group_rank, d->group_rank + G);
     p->hg = hg;
@@ -140,6 +201,7 @@ int dckv_plan_create(const dckv_layer_desc* d, dckv_plan** out) {
     delete p;
     return fail(DCKV_ENOMEM, "plan_create: host allocation failed");
   }
+  dckv::build_mfma_tables(*p);
   *out = p;
   return DCKV_OK;
 }
@@ -165,6 +227,8 @@ int dckv_plan_info(const dckv_plan* p, dckv_plan_geometry* geo, int32_t* koff,
     geo->q_per_kv = p->qpk;
     geo->folded_query_len = p->qlen;
     geo->split_tokens = p->split_tokens;
+    geo->mfma_path = p->mfma_ok ? 1 : 0;
+    geo->head_slices = p->mfma_ok ? p->mfma.n_slices : 0;
     geo->page_elems = p->page_elems;
     geo->value_base = p->value_base;
     geo->key_factor_elems = p->key_factor_elems;

@@ -61,6 +61,15 @@ SMALL = {
     "singletons": dict(hidden=1024, num_q_heads=8, num_kv_heads=8, head_dim=128,
                        sizes=(1, 1, 1, 2, 1, 1, 1), group_rank=(31, 64, 17, 150, 99, 128, 5),
                        value_rank=384, seq_lens=(2049, 65, 640), permute_pages=True, split=512),
+    # 32 heads with two 16-head tiles and odd group boundaries inside tiles
+    "mha32_two_tiles": dict(hidden=1024, num_q_heads=32, num_kv_heads=32, head_dim=64,
+                            sizes=(7, 9, 5, 1, 10), group_rank=(201, 333, 97, 31, 160),
+                            value_rank=512, seq_lens=(700, 1, 64, 383), permute_pages=True,
+                            split=256),
+    # value rank above what the MFMA accumulators hold: the portable bf16 kernels run
+    "valu_bf16": dict(hidden=2560, num_q_heads=32, num_kv_heads=32, head_dim=128,
+                      sizes=(8, 8, 8, 8), group_rank=(300, 200, 100, 50), value_rank=2304,
+                      seq_lens=(200, 70), permute_pages=False, split=128),
 }
 
 

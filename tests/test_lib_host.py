@@ -160,3 +160,19 @@ def test_binding_rejects_host_tensors():
         decode(p, torch.zeros(1, 8, 64), torch.zeros(4, p.page_elems), torch.zeros(1, 4, dtype=torch.int32),
                torch.zeros(1, dtype=torch.int32), 256, torch.zeros(p.key_factor_elems),
                torch.zeros(128, 512))
+
+
+def test_decode_path_selection():
+    expect = {"tiny_mha_f32": 0, "mha7b_b8_t4k": 1, "gqa8b_b4_t32k": 1, "mha_long_t128k": 1,
+              "mha_ragged_b64": 1}
+    for name, mfma in expect.items():
+        assert _plan(make_workload(name)).geometry["mfma_path"] == mfma, name
+    from paper_2607_24331_amd import Plan
+    # value rank 2304 with 32 heads exceeds the MFMA accumulators: portable path
+    p = Plan(2560, 32, 32, 128, [i // 8 for i in range(32)], [300, 200, 100, 50], 2304, "bf16")
+    assert p.geometry["mfma_path"] == 0
+    # explicit head slices
+    wl = make_workload("mha_long_t128k")
+    from paper_2607_24331_amd import Plan as P2
+    p2 = P2(wl.hidden, 32, 32, 128, wl.group_of_kv, wl.group_rank, wl.value_rank, "bf16", 0, 2)
+    assert p2.geometry["mfma_path"] == 1 and p2.geometry["head_slices"] == 2
