@@ -66,9 +66,9 @@ def device_inputs(wl, plan, torch):
     )
     if wl.append_tokens:
         d["x"] = torch.randn((wl.append_tokens, wl.hidden), generator=g, device=dev).to(tdt)
-        d["L_keys"] = (torch.randn((wl.hidden, wl.key_rank_total), generator=g, device=dev)
-                       / math.sqrt(wl.hidden)).to(tdt)
-        d["L_value"] = (torch.randn((wl.hidden, wl.value_rank), generator=g, device=dev)
+        d["L_keys"] = (torch.randn((wl.key_rank_total, wl.hidden), generator=g, device=dev)
+                       / math.sqrt(wl.hidden)).to(tdt)       # [out, in] layout
+        d["L_value"] = (torch.randn((wl.value_rank, wl.hidden), generator=g, device=dev)
                         / math.sqrt(wl.hidden)).to(tdt)
         p0 = wl.prefill_lens[0]
         posn = torch.arange(p0, p0 + wl.append_tokens)

@@ -144,8 +144,10 @@ int dckv_decode_workspace_bytes(const dckv_plan* plan, int32_t batch, int32_t ma
  * III-C and whole-projection L_v of Sec. III-D), computed with fp32
  * accumulation and rounded to nearest-even into the pool.
  *   x        device [n_tok, m] row-major, latent dtype
- *   L_keys   device [m, R_K] row-major = [L_0 | L_1 | ... | L_{G-1}]
- *   L_value  device [m, r_v] row-major
+ *   L_keys   device [R_K, m] row-major: the transpose of [L_0 | L_1 | ... |
+ *            L_{G-1}] (m x R_K), i.e. the [out, in] layout of a linear
+ *            layer's weight; row koff_g + j holds column j of L_g
+ *   L_value  device [r_v, m] row-major: the transpose of L_v (m x r_v)
  *   slot     device int64 [n_tok]: page*64 + slot-in-page of each token;
  *            a negative slot, or one at or beyond num_pages*64, skips the token
  *   pool     device, num_pages * page_elems elements of the latent dtype

@@ -36,7 +36,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kRing = 16;                 // loads in flight per wave
 constexpr int kPageSlots = 256;           // pages per split the LDS page list holds
 constexpr int kPStride = 72;              // bf16 per head row of the p tile (64 + pad)
-constexpr int kMergeRanks = 16;           // value ranks per merge work-group
+constexpr int kMergeRanks = 8;            // value ranks per merge work-group
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -408,90 +408,196 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
 }
 
 // ---------------------------------------------------------------------------
-// Merge: a[b][h][r] = sum_s 2^(m_s - M) acc_s[r] / sum_s 2^(m_s - M) l_s,
-// splits in ascending order.  Grid (rank chunks, batch * slices).
+// Merge: a[b][h][r] = sum_s 2^(m_s - M) acc_s[r] / sum_s 2^(m_s - M) l_s.
+// Grid (value-rank chunks of kMergeRanks, batch * slices), 256 threads.  A
+// split row of the chunk is kMergeRanks * NH contiguous floats; TPR threads
+// cover it with float4 loads (4 head slots each) and the 256 / TPR thread
+// groups take the splits round-robin.  Fixed order: group g sums splits
+// g, g + G, ... in ascending order, then the G group sums are added in order.
+template <int NH>
 __global__ __launch_bounds__(256) void merge_mfma(const float* __restrict__ part,
                                                   const int32_t* __restrict__ seq_lens,
                                                   int max_context, int split_tokens, int n_split,
-                                                  int rv, int nh, float* __restrict__ amerged,
+                                                  int rv, float* __restrict__ amerged,
                                                   HeadTables tb, MfmaTables mt) {
+  constexpr int TPR = kMergeRanks * NH / 4;   // threads a split row
+  constexpr int G = 256 / TPR;                // split groups
+  constexpr int SUB = 256 / NH;               // split groups of the max / sum pass
   const int rc = blockIdx.x;
   const int bj = blockIdx.y;
   const int J = mt.n_slices;
   const int b = bj / J, slice = bj % J;
   const int tid = threadIdx.x;
-  __shared__ float sM[32], sInvL[32];
+  __shared__ float red[256];
+  __shared__ float sM[NH], sInvL[NH];
+  __shared__ float4 racc[256];
   int T_b = seq_lens[b];
   T_b = T_b < 0 ? 0 : (T_b > max_context ? max_context : T_b);
   const int ns = (T_b + split_tokens - 1) / split_tokens;
-  const int64_t stride = int64_t(nh) * (2 + rv);
+  const int64_t stride = int64_t(NH) * (2 + rv);
   const float* pb = part + (int64_t(b) * J + slice) * n_split * stride;
-  if (tid < nh) {
-    float M = -INFINITY;
-    for (int s = 0; s < ns; ++s) M = fmaxf(M, pb[s * stride + tid]);
-    float L = 0.f;
-    if (M != -INFINITY)
-      for (int s = 0; s < ns; ++s) L += exp2f(pb[s * stride + tid] - M) * pb[s * stride + nh + tid];
-    sM[tid] = M;
-    sInvL[tid] = (L > 0.f) ? 1.f / L : 0.f;
-  }
-  __syncthreads();
-  const int r0 = rc * kMergeRanks;
-  for (int e = tid; e < kMergeRanks * nh; e += 256) {
-    const int hp = e % nh, r = r0 + e / nh;
-    const int h = mt.hord[slice][hp];
-    if (r >= rv || h < 0) continue;
-    const float M = sM[hp];
-    float a = 0.f;
-    if (M != -INFINITY) {
-      const float* src = pb + 2 * nh + int64_t(r) * nh + hp;
-      int s = 0;
-      for (; s + 4 <= ns; s += 4) {
-        const float m0 = pb[(s + 0) * stride + hp], m1 = pb[(s + 1) * stride + hp];
-        const float m2 = pb[(s + 2) * stride + hp], m3 = pb[(s + 3) * stride + hp];
-        const float a0 = src[(s + 0) * stride], a1 = src[(s + 1) * stride];
-        const float a2 = src[(s + 2) * stride], a3 = src[(s + 3) * stride];
-        a = fmaf(exp2f(m0 - M), a0, a);
-        a = fmaf(exp2f(m1 - M), a1, a);
-        a = fmaf(exp2f(m2 - M), a2, a);
-        a = fmaf(exp2f(m3 - M), a3, a);
-      }
-      for (; s < ns; ++s) a = fmaf(exp2f(pb[s * stride + hp] - M), src[s * stride], a);
-      a *= sInvL[hp];
+
+  // pass 1: per head slot maximum, then the weighted sum of l
+  {
+    const int h = tid % NH, sub = tid / NH;
+    float mx = -INFINITY;
+    for (int s = sub; s < ns; s += SUB) mx = fmaxf(mx, pb[s * stride + h]);
+    red[tid] = mx;
+    __syncthreads();
+    if (tid < NH) {
+      float M = -INFINITY;
+      for (int k = 0; k < SUB; ++k) M = fmaxf(M, red[k * NH + tid]);
+      sM[tid] = M;
     }
-    amerged[(int64_t(b) * tb.n_q_heads + h) * rv + r] = a;
+    __syncthreads();
+    const float M = sM[h];
+    float l = 0.f;
+    if (M != -INFINITY)
+      for (int s = sub; s < ns; s += SUB) l += exp2f(pb[s * stride + h] - M) * pb[s * stride + NH + h];
+    red[tid] = l;
+    __syncthreads();
+    if (tid < NH) {
+      float L = 0.f;
+      for (int k = 0; k < SUB; ++k) L += red[k * NH + tid];
+      sInvL[tid] = L > 0.f ? 1.f / L : 0.f;
+    }
+    __syncthreads();
+  }
+
+  // pass 2: weighted sum of the chunk's accumulators
+  const int g = tid / TPR, e = tid % TPR;
+  const int rl = e / (NH / 4);                 // rank inside the chunk
+  const int hq = (e % (NH / 4)) * 4;           // first of four head slots
+  const int r = rc * kMergeRanks + rl;
+  const float4 M4 = make_float4(sM[hq], sM[hq + 1], sM[hq + 2], sM[hq + 3]);
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (r < rv) {
+    const float* src = pb + 2 * NH + int64_t(r) * NH + hq;
+    int s = g;
+    for (; s + 3 * G < ns; s += 4 * G) {
+      float4 mv[4], av[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        mv[k] = *reinterpret_cast<const float4*>(pb + (s + k * G) * stride + hq);
+        av[k] = *reinterpret_cast<const float4*>(src + (s + k * G) * stride);
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        a.x = fmaf(exp2f(mv[k].x - M4.x), av[k].x, a.x);
+        a.y = fmaf(exp2f(mv[k].y - M4.y), av[k].y, a.y);
+        a.z = fmaf(exp2f(mv[k].z - M4.z), av[k].z, a.z);
+        a.w = fmaf(exp2f(mv[k].w - M4.w), av[k].w, a.w);
+      }
+    }
+    for (; s < ns; s += G) {
+      const float4 mv = *reinterpret_cast<const float4*>(pb + s * stride + hq);
+      const float4 av = *reinterpret_cast<const float4*>(src + s * stride);
+      a.x = fmaf(exp2f(mv.x - M4.x), av.x, a.x);
+      a.y = fmaf(exp2f(mv.y - M4.y), av.y, a.y);
+      a.z = fmaf(exp2f(mv.z - M4.z), av.z, a.z);
+      a.w = fmaf(exp2f(mv.w - M4.w), av.w, a.w);
+    }
+  }
+  racc[tid] = a;
+  __syncthreads();
+  if (g == 0 && r < rv) {
+    float4 t = racc[e];
+    for (int k = 1; k < G; ++k) {
+      const float4 u = racc[k * TPR + e];
+      t.x += u.x;
+      t.y += u.y;
+      t.z += u.z;
+      t.w += u.w;
+    }
+    const float tv[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int h = mt.hord[slice][hq + k];
+      if (h >= 0)
+        amerged[(int64_t(b) * tb.n_q_heads + h) * rv + r] =
+            sM[hq + k] == -INFINITY ? 0.f : tv[k] * sInvL[hq + k];
+    }
   }
 }
 
-// Up-projection o[b][h][d] = sum_r a[b][h][r] R_v[r][kv(h)*d_h + d].
-// Grid (query heads, batch); 256 threads = d columns x rank quarters.
+// Up-projection o[b][h][:] = a[b][h][:] R_v[:, kv(h) block] (Sec. III-A z R,
+// Sec. III-D R_v).  Grid (KV heads, column tiles of 32, row blocks of 8): a
+// work-group serves every query row (sequence, head) of its KV head in its row
+// block, for 32 output columns.  Thread t: 8 columns (one 16-byte load a
+// rank), rank group t/4 (ranks t/4, t/4 + 64, ...), four loads in flight; the
+// 64 rank groups are then summed in a fixed order, one query row a round.
 __global__ __launch_bounds__(256) void upproj(const float* __restrict__ amerged,
                                               const bf16* __restrict__ Rv,
-                                              float* __restrict__ out, int rv, HeadTables tb) {
-  const int h = blockIdx.x, b = blockIdx.y;
+                                              float* __restrict__ out, int batch, int rv,
+                                              HeadTables tb) {
+  constexpr int RB = 8;                        // query rows a work-group
+  constexpr int U = 4;                         // loads in flight a thread
+  const int kv = blockIdx.x, ct = blockIdx.y, rbk = blockIdx.z;
   const int tid = threadIdx.x;
-  const int dh = tb.head_dim, n = tb.n_kv_heads * dh;
-  const int kv = h / tb.q_per_kv;
-  __shared__ float sa[DCKV_MAX_VALUE_RANK];
-  __shared__ float red[256];
-  const float* a = amerged + (int64_t(b) * tb.n_q_heads + h) * rv;
-  for (int r = tid; r < rv; r += 256) sa[r] = a[r];
+  const int dh = tb.head_dim, n = tb.n_kv_heads * dh, qpk = tb.q_per_kv;
+  const int rows = batch * qpk;
+  const int row0 = rbk * RB;
+  const int nrow = min(RB, rows - row0);
+  if (nrow <= 0) return;
+  extern __shared__ float sa[];                // [RB][rv]
+  __shared__ float red[64][33];
+  for (int i = tid; i < nrow * rv; i += 256) {
+    const int q = i / rv, r = i - q * rv;
+    const int row = row0 + q;
+    const int b = row / qpk, h = kv * qpk + row % qpk;
+    sa[q * rv + r] = amerged[(int64_t(b) * tb.n_q_heads + h) * rv + r];
+  }
   __syncthreads();
-  // thread -> (column d, rank group); 2 columns a thread when d_h > 128
-  const int groups = 256 / min(256, dh);
-  for (int d0 = 0; d0 < dh; d0 += 256 / groups) {
-    const int d = d0 + tid % (256 / groups), g = tid / (256 / groups);
-    float acc = 0.f;
-    if (d < dh) {
-      const bf16* col = Rv + int64_t(kv) * dh + d;
-      for (int r = g; r < rv; r += groups) acc = fmaf(sa[r], static_cast<float>(col[int64_t(r) * n]), acc);
+  const int c8 = tid % 4, rg = tid / 4;
+  const int col = ct * 32 + 8 * c8;            // first of eight output columns
+  float acc[RB][8];
+#pragma unroll
+  for (int q = 0; q < RB; ++q)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[q][j] = 0.f;
+  auto fma8 = [&](const u32x4 v, int r) {
+    float f[8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      f[2 * j] = __uint_as_float(v[j] << 16);
+      f[2 * j + 1] = __uint_as_float(v[j] & 0xFFFF0000u);
     }
-    red[tid] = acc;
+#pragma unroll
+    for (int q = 0; q < RB; ++q) {
+      if (q < nrow) {
+        const float aq = sa[q * rv + r];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[q][j] = fmaf(aq, f[j], acc[q][j]);
+      }
+    }
+  };
+  if (col < dh) {                              // d_h is a multiple of 8 on this path
+    const bf16* src = Rv + int64_t(kv) * dh + col;
+    int r = rg;
+    for (; r + (U - 1) * 64 < rv; r += U * 64) {
+      u32x4 v[U];
+#pragma unroll
+      for (int k = 0; k < U; ++k) v[k] = load16(src + int64_t(r + 64 * k) * n);
+#pragma unroll
+      for (int k = 0; k < U; ++k) fma8(v[k], r + 64 * k);
+    }
+    for (; r < rv; r += 64) fma8(load16(src + int64_t(r) * n), r);
+  }
+#pragma unroll
+  for (int q = 0; q < RB; ++q) {
+    if (q >= nrow) break;                      // block-uniform
+#pragma unroll
+    for (int j = 0; j < 8; ++j) red[rg][8 * c8 + j] = acc[q][j];
     __syncthreads();
-    if (g == 0 && d < dh) {
-      float o = 0.f;
-      for (int k = 0; k < groups; ++k) o += red[k * (256 / groups) + tid % (256 / groups)];
-      out[(int64_t(b) * tb.n_q_heads + h) * dh + d] = o;
+    if (tid < 32) {
+      float t = red[0][tid];
+      for (int k = 1; k < 64; ++k) t += red[k][tid];
+      const int cc = ct * 32 + tid;
+      if (cc < dh) {
+        const int row = row0 + q;
+        const int b = row / qpk, h = kv * qpk + row % qpk;
+        out[(int64_t(b) * tb.n_q_heads + h) * dh + cc] = t;
+      }
     }
     __syncthreads();
   }
@@ -560,13 +666,23 @@ hipError_t launch_decode_mfma(const dckv_plan& p, const DecodeShape& sh, const f
             : launch_split_w<8, 2>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part, lds, stream);
   if (e != hipSuccess) return e;
   if (p.prof_after && (e = hipEventRecord(p.prof_after, stream)) != hipSuccess) return e;
-  const int nh = 16 * p.mfma.nt;
-  hipLaunchKernelGGL(merge_mfma, dim3(sh.n_rchunks, sh.batch * p.mfma.n_slices), dim3(256), 0,
-                     stream, part, seq_lens, sh.max_context, sh.split_tokens, sh.n_split, p.rv, nh,
-                     amerged, p.tables, p.mfma);
+  if (p.mfma.nt == 1)
+    hipLaunchKernelGGL(merge_mfma<16>, dim3(sh.n_rchunks, sh.batch * p.mfma.n_slices), dim3(256), 0,
+                       stream, part, seq_lens, sh.max_context, sh.split_tokens, sh.n_split, p.rv,
+                       amerged, p.tables, p.mfma);
+  else
+    hipLaunchKernelGGL(merge_mfma<32>, dim3(sh.n_rchunks, sh.batch * p.mfma.n_slices), dim3(256), 0,
+                       stream, part, seq_lens, sh.max_context, sh.split_tokens, sh.n_split, p.rv,
+                       amerged, p.tables, p.mfma);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(upproj, dim3(p.Hq, sh.batch), dim3(256), 0, stream, amerged,
-                     static_cast<const bf16*>(R_value), out, p.rv, p.tables);
+  const int rows = sh.batch * p.qpk;
+  const size_t lds_up = size_t(8) * p.rv * sizeof(float);
+  e = hipFuncSetAttribute(reinterpret_cast<const void*>(upproj),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, int(lds_up));
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(upproj, dim3(p.Hkv, (p.dh + 31) / 32, (rows + 7) / 8), dim3(256), lds_up,
+                     stream, amerged, static_cast<const bf16*>(R_value), out, sh.batch, p.rv,
+                     p.tables);
   return hipGetLastError();
 }
 

@@ -35,6 +35,7 @@ void build_mfma_tables(dckv_plan& p) {
   p.mfma_ok = false;
   p.mfma = MfmaTables{};
   if (p.dtype != DCKV_BF16) return;
+  if (p.dh % 8 != 0) return;                   // the up-projection reads 8 columns at a time
   MfmaTables& t = p.mfma;
   // Query heads ordered by (group of their KV head, head index): the heads
   // of one group are adjacent, so a tile's key columns are one range.

@@ -146,12 +146,14 @@ def _num_pages(plan: Plan, pool: torch.Tensor) -> int:
 
 def latent_append(plan: Plan, x: torch.Tensor, L_keys: torch.Tensor, L_value: torch.Tensor,
                   slot: torch.Tensor, pool: torch.Tensor, stream=None) -> None:
-    """Write z = x [L_keys | L_value] of each row of x into its pool slot."""
+    """Write z = x L of each row of x into its pool slot.  L_keys [R_K, m] and
+    L_value [r_v, m] hold the factors transposed ([out, in], as a linear
+    layer's weight)."""
     n_tok = x.shape[0] if x.dim() == 2 else -1
     dt = plan.torch_dtype
     px = _dev(x, "x", dt, (n_tok, plan.hidden))
-    pk = _dev(L_keys, "L_keys", dt, (plan.hidden, plan.key_rank_total))
-    pv = _dev(L_value, "L_value", dt, (plan.hidden, plan.value_rank))
+    pk = _dev(L_keys, "L_keys", dt, (plan.key_rank_total, plan.hidden))
+    pv = _dev(L_value, "L_value", dt, (plan.value_rank, plan.hidden))
     ps = _dev(slot, "slot", torch.int64, (n_tok,))
     pp = _dev(pool, "pool", dt)
     _check(_lib.dckv_latent_append(plan.handle, px, n_tok, pk, pv, ps, pp, _num_pages(plan, pool),

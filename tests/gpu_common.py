@@ -58,8 +58,8 @@ def gpu_pool_with_append(inp: Inputs, plan):
     wl = inp.wl
     pool = dev(oracle_pool(inp, with_append=False), wl.dtype)
     if wl.append_tokens:
-        latent_append(plan, dev(inp.x, wl.dtype), dev(inp.L_keys, wl.dtype), dev(inp.L_value, wl.dtype),
-                      torch.from_numpy(append_slots(inp)).cuda(), pool)
+        latent_append(plan, dev(inp.x, wl.dtype), dev(inp.L_keys.T, wl.dtype),
+                      dev(inp.L_value.T, wl.dtype), torch.from_numpy(append_slots(inp)).cuda(), pool)
     return pool
 
 

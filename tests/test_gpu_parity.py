@@ -209,7 +209,7 @@ def test_append_layout_bit_exact_on_exact_inputs():
     plan = plan_for(wl, split)
     from paper_2607_24331_amd import latent_append
     pool = dev(np.full(ref.shape, sentinel, np.float32), "bf16")
-    latent_append(plan, dev(x, "bf16"), dev(Lk, "bf16"), dev(Lv, "bf16"),
+    latent_append(plan, dev(x, "bf16"), dev(Lk.T, "bf16"), dev(Lv.T, "bf16"),
                   torch.from_numpy(slots).cuda(), pool)
     torch.cuda.synchronize()
     got_bits = pool.view(torch.int16).cpu().numpy().view(np.uint16)
@@ -230,7 +230,7 @@ def test_append_random_within_one_ulp():
     plan = plan_for(wl, split)
     from paper_2607_24331_amd import latent_append
     pool = plan.new_pool(6)
-    latent_append(plan, dev(x, "bf16"), dev(Lk, "bf16"), dev(Lv, "bf16"),
+    latent_append(plan, dev(x, "bf16"), dev(Lk.T, "bf16"), dev(Lv.T, "bf16"),
                   torch.from_numpy(slots).cuda(), pool)
     torch.cuda.synchronize()
     Zk_g, Zv_g = olayout.unpack(pool.float().cpu().numpy(), table, 0, n, wl.key_rank_total, wl.value_rank)
@@ -278,3 +278,34 @@ def test_full_workload_sampled_rows(name):
     errs = [row_rel_err(out[b, h], ref[(b, h)]) for b, h in pairs]
     _report(name, errs)
     assert max(errs) <= TOL_REL_ROW
+
+
+@pytest.mark.parametrize("hidden", [200, 512])
+def test_append_bf16_both_kernels(hidden):
+    # hidden 200 (not a multiple of 32) takes the portable kernel, 512 the MFMA one
+    wl = custom_workload(name="append_h", seed=77, hidden=hidden, num_q_heads=4, num_kv_heads=4,
+                         head_dim=64, group_of_kv=(0, 1, 1, 0), group_rank=(50, 61), value_rank=100,
+                         dtype="bf16", batch=1, seq_lens=(130,), prefill_lens=(130,))
+    g = np.random.default_rng(5)
+    from workloads.inputs import to_storage
+    n = 130
+    x = to_storage(g.standard_normal((n, hidden)), "bf16")
+    Lk = to_storage(g.standard_normal((hidden, 111)) / np.sqrt(hidden), "bf16")
+    Lv = to_storage(g.standard_normal((hidden, 100)) / np.sqrt(hidden), "bf16")
+    perm = np.random.default_rng(6).permutation(3).astype(np.int32)
+    table = perm[None, :]
+    pos = np.arange(n)
+    slots = table[0, pos // 64].astype(np.int64) * 64 + pos % 64
+    plan = plan_for(wl)
+    from paper_2607_24331_amd import latent_append
+    pool = plan.new_pool(3)
+    latent_append(plan, dev(x, "bf16"), dev(Lk.T, "bf16"), dev(Lv.T, "bf16"),
+                  torch.from_numpy(slots).cuda(), pool)
+    torch.cuda.synchronize()
+    Zk_g, Zv_g = olayout.unpack(pool.float().cpu().numpy(), table, 0, n, 111, 100)
+    for Zg, L in ((Zk_g, Lk), (Zv_g, Lv)):
+        exact = oappend.down_project(x, L)
+        rounded = obf16.round_to_bf16(exact)
+        bound = obf16.ulp_bf16(rounded) + hidden * 2.0 ** -24 * oappend.abs_bound(x, L)
+        assert np.all(np.abs(Zg - rounded) <= bound)
+        assert np.mean(Zg == rounded) > 0.99
