@@ -36,7 +36,11 @@ def parse():
     ap.add_argument("--workload", default="mha_long_t128k")
     ap.add_argument("--split-tokens", type=int, default=0)
     ap.add_argument("--head-slices", type=int, default=0)
+    ap.add_argument("--decode-waves", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="run one device copy of this many MiB before timing (a known-size "
+                         "kernel for scaling hardware traffic counters)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle sample")
     return ap.parse_args()
@@ -167,7 +171,8 @@ def main():
 
     wl = make_workload(args.workload)
     plan = Plan(wl.hidden, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_of_kv,
-                wl.group_rank, wl.value_rank, wl.dtype, args.split_tokens, args.head_slices)
+                wl.group_rank, wl.value_rank, wl.dtype, args.split_tokens, args.head_slices,
+                args.decode_waves)
     mfma = bool(plan.geometry["mfma_path"])
     inp = device_inputs(wl, plan, torch)
     max_ctx = max(wl.seq_lens)
@@ -181,6 +186,13 @@ def main():
         decode(plan, inp["q"], inp["pool"], inp["page_table"], inp["seq_lens"], max_ctx,
                inp["R_keys"], inp["R_value"], out=out, workspace=ws)
 
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -234,6 +246,7 @@ def main():
             "group_ranks": list(wl.group_rank), "value_rank": wl.value_rank,
             "latent_dtype": wl.dtype, "split_tokens": split_used,
             "head_slices": plan.geometry["head_slices"],
+            "decode_waves": plan.geometry["decode_waves"],
         },
         "context_tokens_per_s": sum(wl.seq_lens) / (ms_step * 1e-3),
         "step_hbm_gbs": (nb["decode_total"] + nb["append"]) / (ms_step * 1e-3) / 1e9,

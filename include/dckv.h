@@ -26,11 +26,13 @@
  *     koff_g = r_0 + ... + r_{g-1}.
  *
  * Paged cache layout (64 tokens per page; R_K = sum_g r_g; R_Kp = R_K
- * rounded up to a multiple of 8; page_elems = 64*R_Kp + 64*r_v elements of
+ * rounded up to a multiple of 32; page_elems = 64*R_Kp + 64*r_v elements of
  * the latent dtype):
- *   key part    token-major [64][R_Kp]: (slot s, key column k) at s*R_Kp + k;
- *               columns R_K..R_Kp-1 are written as zero by dckv_latent_append
- *   value part  rank-major  [r_v][64]: (slot s, value column j) at
+ *   key part    chunk-major: key columns in chunks of 32, each chunk holding
+ *               the 64 slots one after another: (slot s, key column k) at
+ *               (k/32)*2048 + s*32 + k%32; columns R_K..R_Kp-1 are written
+ *               as zero by dckv_latent_append
+ *   value part  rank-major [r_v][64]: (slot s, value column j) at
  *               64*R_Kp + j*64 + s
  *   Position pos of sequence b lives in page page_table[b*max_pages + pos/64],
  *   slot pos%64.  Page p starts at element p*page_elems of the pool.
@@ -95,18 +97,22 @@ typedef struct dckv_layer_desc {
   int32_t head_slices;             /* query-head slices served by separate decode
                                       work-groups (bf16 path); 0 for the default
                                       (one slice per 32 heads) */
+  int32_t decode_waves;            /* waves of a bf16 decode work-group: 4 or 8,
+                                      or 0 for the default (fewest that keep the
+                                      accumulators within 128 registers a lane) */
 } dckv_layer_desc;
 
 /* Derived layout facts of a plan. */
 typedef struct dckv_plan_geometry {
   int32_t key_rank_total;          /* R_K = sum of r_g */
-  int32_t key_row_stride;          /* R_Kp: R_K rounded up to a multiple of 8 */
+  int32_t key_width_padded;        /* R_Kp: R_K rounded up to a multiple of 32 */
   int32_t value_rank;              /* r_v */
   int32_t q_per_kv;                /* H_q / H_kv */
   int32_t folded_query_len;        /* sum over query heads h of r_{g(h)} */
   int32_t split_tokens;            /* tokens per decode split as described (0: per call) */
   int32_t mfma_path;               /* 1 if decode uses the bf16 MFMA kernels */
   int32_t head_slices;             /* query-head slices of the MFMA path (0 otherwise) */
+  int32_t decode_waves;            /* waves a decode work-group on the MFMA path (0 otherwise) */
   int64_t page_elems;              /* elements per page: 64*R_Kp + 64*r_v */
   int64_t value_base;              /* element offset of the value part in a page: 64*R_Kp */
   int64_t key_factor_elems;        /* elements of the concatenated R_g blocks */

@@ -2,18 +2,21 @@
 token, Sec. III-A, but fixes no memory layout).
 
 A pool is an array of pages; a page holds 64 consecutive token positions of
-one sequence.  With R_K the total key rank and r_v the value rank, a page of
+one sequence.  With R_K the total key rank and r_v the value rank, let
+R_Kp = R_K rounded up to a multiple of 32.  A page of
 page_elems = 64 * R_Kp + 64 * r_v elements holds
 
-  key part    [64 slots][R_Kp] token-major: element (slot s, key column k)
-              at s * R_Kp + k; columns R_K .. R_Kp-1 are zero padding;
-              group g's latent is columns koff_g .. koff_g + r_g - 1
-  value part  [r_v][64] rank-major: element (slot s, value column j)
-              at 64 * R_Kp + j * 64 + s
+  key part    chunk-major: key columns in chunks of 32; chunk c holds the 64
+              slots one after another, 32 columns each.  Element (slot s,
+              key column k) sits at (k // 32) * 2048 + s * 32 + k % 32.
+              Columns R_K .. R_Kp-1 are zero padding.  Group g's latent is
+              columns koff_g .. koff_g + r_g - 1.
+  value part  rank-major [r_v][64]: element (slot s, value column j) at
+              64 * R_Kp + j * 64 + s
 
-with R_Kp = R_K rounded up to a multiple of 8.  Token position pos of
-sequence b lives in physical page page_table[b][pos // 64], slot pos % 64.
-Slots past a sequence's length hold zeros in a freshly packed pool.
+Token position pos of sequence b lives in physical page page_table[b][pos // 64],
+slot pos % 64.  Slots past a sequence's length hold zeros in a freshly packed
+pool.
 """
 
 from __future__ import annotations
@@ -21,25 +24,26 @@ from __future__ import annotations
 import numpy as np
 
 PAGE_TOKENS = 64
+KEY_CHUNK = 32
 
 
-def key_row_stride(key_rank_total: int) -> int:
-    return -(-key_rank_total // 8) * 8
+def key_width_padded(key_rank_total: int) -> int:
+    return -(-key_rank_total // KEY_CHUNK) * KEY_CHUNK
 
 
 def page_elems(key_rank_total: int, value_rank: int) -> int:
-    return PAGE_TOKENS * key_row_stride(key_rank_total) + PAGE_TOKENS * value_rank
+    return PAGE_TOKENS * key_width_padded(key_rank_total) + PAGE_TOKENS * value_rank
 
 
 def value_base(key_rank_total: int) -> int:
-    return PAGE_TOKENS * key_row_stride(key_rank_total)
+    return PAGE_TOKENS * key_width_padded(key_rank_total)
 
 
-def key_offset(slot: int, k: int, key_rank_total: int) -> int:
-    return slot * key_row_stride(key_rank_total) + k
+def key_offset(slot, k, key_rank_total: int):
+    return (k // KEY_CHUNK) * (PAGE_TOKENS * KEY_CHUNK) + slot * KEY_CHUNK + k % KEY_CHUNK
 
 
-def value_offset(slot: int, j: int, key_rank_total: int) -> int:
+def value_offset(slot, j, key_rank_total: int):
     return value_base(key_rank_total) + j * PAGE_TOKENS + slot
 
 
@@ -48,10 +52,19 @@ def new_pool(num_pages: int, key_rank_total: int, value_rank: int, dtype=np.floa
 
 
 def _page_views(pool, page, R_K, r_v):
-    RKp = key_row_stride(R_K)
-    keys = pool[page, :PAGE_TOKENS * RKp].reshape(PAGE_TOKENS, RKp)
+    """Views of one page: keys [chunks][64][32] and values [r_v][64]."""
+    RKp = key_width_padded(R_K)
+    keys = pool[page, :PAGE_TOKENS * RKp].reshape(RKp // KEY_CHUNK, PAGE_TOKENS, KEY_CHUNK)
     vals = pool[page, PAGE_TOKENS * RKp:PAGE_TOKENS * RKp + PAGE_TOKENS * r_v].reshape(r_v, PAGE_TOKENS)
     return keys, vals
+
+
+def _chunked(Z: np.ndarray, RKp: int) -> np.ndarray:
+    """[T, R_K] -> [chunks][T][32], zero-padded to R_Kp columns."""
+    T, R_K = Z.shape
+    full = np.zeros((T, RKp), dtype=Z.dtype)
+    full[:, :R_K] = Z
+    return full.reshape(T, RKp // KEY_CHUNK, KEY_CHUNK).transpose(1, 0, 2)
 
 
 def pack(pool: np.ndarray, page_table: np.ndarray, b: int, start: int,
@@ -68,7 +81,7 @@ def pack(pool: np.ndarray, page_table: np.ndarray, b: int, start: int,
         t0 = pos - start
         t1 = t0 + (s1 - s0)
         keys, vals = _page_views(pool, page, R_K, r_v)
-        keys[s0:s1, :R_K] = Zk[t0:t1]
+        keys[:, s0:s1, :] = _chunked(Zk[t0:t1], keys.shape[0] * KEY_CHUNK)
         vals[:, s0:s1] = Zv[t0:t1].T
         pos += s1 - s0
 
@@ -82,6 +95,7 @@ def unpack(pool: np.ndarray, page_table: np.ndarray, b: int, T: int,
         page = int(page_table[b, p])
         s1 = min(PAGE_TOKENS, T - p * PAGE_TOKENS)
         keys, vals = _page_views(pool, page, key_rank_total, value_rank)
-        Zk[p * PAGE_TOKENS:p * PAGE_TOKENS + s1] = keys[:s1, :key_rank_total]
+        rows = keys[:, :s1, :].transpose(1, 0, 2).reshape(s1, -1)
+        Zk[p * PAGE_TOKENS:p * PAGE_TOKENS + s1] = rows[:, :key_rank_total]
         Zv[p * PAGE_TOKENS:p * PAGE_TOKENS + s1] = vals[:, :s1].T
     return Zk, Zv

@@ -42,19 +42,21 @@ class LayerDesc(ctypes.Structure):
         ("latent_dtype", ctypes.c_int32),
         ("split_tokens", ctypes.c_int32),
         ("head_slices", ctypes.c_int32),
+        ("decode_waves", ctypes.c_int32),
     ]
 
 
 class PlanGeometry(ctypes.Structure):
     _fields_ = [
         ("key_rank_total", ctypes.c_int32),
-        ("key_row_stride", ctypes.c_int32),
+        ("key_width_padded", ctypes.c_int32),
         ("value_rank", ctypes.c_int32),
         ("q_per_kv", ctypes.c_int32),
         ("folded_query_len", ctypes.c_int32),
         ("split_tokens", ctypes.c_int32),
         ("mfma_path", ctypes.c_int32),
         ("head_slices", ctypes.c_int32),
+        ("decode_waves", ctypes.c_int32),
         ("page_elems", ctypes.c_int64),
         ("value_base", ctypes.c_int64),
         ("key_factor_elems", ctypes.c_int64),

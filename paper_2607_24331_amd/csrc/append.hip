@@ -3,7 +3,7 @@
 // accumulated in fp32, rounded to nearest-even into the paged pool.
 //
 // Output column space of one token: [0, R_Kp + r_v)
-//   c <  R_K          key column c           -> page key row, column c
+//   c <  R_K          key column c           -> page key part (chunk-major)
 //   R_K <= c < R_Kp   key-row padding         -> written as zero
 //   c >= R_Kp         value column c - R_Kp   -> page value part, rank-major
 #include "device.h"
@@ -11,6 +11,11 @@
 
 namespace dckv {
 namespace {
+
+// Chunk-major key part: column c of slot s at (c/32)*2048 + s*32 + c%32.
+__device__ __forceinline__ int64_t key_elem(int s, int c) {
+  return int64_t(c >> 5) * (32 * DCKV_PAGE_TOKENS) + s * 32 + (c & 31);
+}
 
 constexpr int kTileTok = 64;
 constexpr int kTileCol = 64;
@@ -86,29 +91,33 @@ __global__ __launch_bounds__(256) void append_valu(const T* __restrict__ x, cons
       const int c = col0 + tx * 4 + j;
       if (c >= ncols) continue;
       if (c < RK)
-        pg[int64_t(s) * RKp + c] = from_f32<T>(acc[i][j]);
+        pg[key_elem(s, c)] = from_f32<T>(acc[i][j]);
       else if (c < RKp)
-        pg[int64_t(s) * RKp + c] = from_f32<T>(0.f);
+        pg[key_elem(s, c)] = from_f32<T>(0.f);
       else
         pg[value_base + int64_t(c - RKp) * DCKV_PAGE_TOKENS + s] = from_f32<T>(acc[i][j]);
     }
   }
 }
 
-// bf16 MFMA kernel (m a multiple of 32).  Output C[token][column] =
-// sum_k x[token][k] * LT[column][k]: both operands are contiguous in k, so
-// every MFMA operand lane reads its 8 consecutive k with one 16-byte load.
-// Work-group tile 64 tokens x 128 columns, four waves of 32 x 64 (2 x 4
-// tiles of 16 x 16), k-steps of 32 with the next step's operands loaded
-// while the current one multiplies.  Rows past the token count or the
-// column space are clamped to valid rows and their results discarded, so no
-// load leaves its matrix.
+// bf16 MFMA kernel (m a multiple of 64).  Output C[token][column] =
+// sum_k x[token][k] * LT[column][k]: both operands are contiguous in k.
+// Work-group tile 128 tokens x 128 columns, four waves of 64 x 64 (4 x 4
+// tiles of 16 x 16); k advances in stages of 64 staged through LDS (rows
+// padded to 72 elements so the 16 rows an MFMA operand load touches fall in
+// distinct banks), two stages in flight: the next stage's global loads are
+// issued before the current stage multiplies.  Rows past the token count or
+// the column space are clamped to valid rows and their results discarded,
+// so no load leaves its matrix.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kAM = 2;   // 16-token tiles a wave
-constexpr int kAN = 4;   // 16-column tiles a wave
+constexpr int kBM = 128;                  // tokens a work-group
+constexpr int kBN = 128;                  // columns a work-group
+constexpr int kBK = 64;                   // k a stage
+constexpr int kLdsRow = kBK + 8;          // padded LDS row (elements)
+constexpr int kStageElems = (kBM + kBN) * kLdsRow;
 
 __global__ __launch_bounds__(256) void append_mfma(const bf16* __restrict__ x,
                                                    const bf16* __restrict__ LkT,
@@ -117,86 +126,108 @@ __global__ __launch_bounds__(256) void append_mfma(const bf16* __restrict__ x,
                                                    bf16* __restrict__ pool, int n_tok, int m, int RK,
                                                    int RKp, int rv, int64_t page_elems,
                                                    int64_t value_base, int64_t num_pages) {
+  __shared__ __align__(16) bf16 lds[2 * kStageElems];
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 15, lq = lane >> 4;
   const int ncols = RKp + rv;
-  const int tok_w = blockIdx.y * 64 + (w >> 1) * 32;
-  const int col_w = blockIdx.x * 128 + (w & 1) * 64;
+  const int tok0 = blockIdx.y * kBM, col0 = blockIdx.x * kBN;
 
-  const bf16* arow[kAM];
+  // global rows this thread stages: rows tid/8 + 32*i (i < 4) of the A and
+  // B tiles, 16-byte piece tid%8 of the stage's 64 k
+  const int piece = tid & 7, prow = tid >> 3;
+  const bf16* ga[4];
+  const bf16* gb[4];
 #pragma unroll
-  for (int i = 0; i < kAM; ++i) {
-    const int t = min(tok_w + 16 * i + lr, n_tok - 1);
-    arow[i] = x + int64_t(t) * m + 8 * lq;
-  }
-  const bf16* brow[kAN];
-#pragma unroll
-  for (int j = 0; j < kAN; ++j) {
-    const int c = col_w + 16 * j + lr;
+  for (int i = 0; i < 4; ++i) {
+    const int t = min(tok0 + prow + 32 * i, n_tok - 1);
+    ga[i] = x + int64_t(t) * m + 8 * piece;
+    const int c = col0 + prow + 32 * i;
     const bf16* r;
     if (c < RK)
       r = LkT + int64_t(c) * m;
     else if (c < RKp)
-      r = LkT;                                  // padding column: written as zero below
+      r = LkT;                                // padding column: written as zero below
     else
       r = LvT + int64_t(min(c - RKp, rv - 1)) * m;
-    brow[j] = r + 8 * lq;
+    gb[i] = r + 8 * piece;
   }
-
-  floatx4_t acc[kAM][kAN];
+  u32x4_t ra[4], rb[4];
+  auto gload = [&](int k) {
 #pragma unroll
-  for (int i = 0; i < kAM; ++i)
-#pragma unroll
-    for (int j = 0; j < kAN; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-
-  u32x4_t a0[kAM], b0[kAN], a1[kAM], b1[kAN];
-  auto load = [&](u32x4_t (&a)[kAM], u32x4_t (&b)[kAN], int k) {
-#pragma unroll
-    for (int i = 0; i < kAM; ++i) a[i] = *reinterpret_cast<const u32x4_t*>(arow[i] + k);
-#pragma unroll
-    for (int j = 0; j < kAN; ++j) b[j] = *reinterpret_cast<const u32x4_t*>(brow[j] + k);
+    for (int i = 0; i < 4; ++i) {
+      ra[i] = *reinterpret_cast<const u32x4_t*>(ga[i] + k);
+      rb[i] = *reinterpret_cast<const u32x4_t*>(gb[i] + k);
+    }
   };
-  auto mma = [&](const u32x4_t (&a)[kAM], const u32x4_t (&b)[kAN]) {
+  auto lstore = [&](int buf) {
+    bf16* A = lds + buf * kStageElems;
+    bf16* B = A + kBM * kLdsRow;
 #pragma unroll
-    for (int i = 0; i < kAM; ++i)
-#pragma unroll
-      for (int j = 0; j < kAN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a[i]),
-                                                            __builtin_bit_cast(bf16x8_t, b[j]),
-                                                            acc[i][j], 0, 0, 0);
+    for (int i = 0; i < 4; ++i) {
+      *reinterpret_cast<u32x4_t*>(A + (prow + 32 * i) * kLdsRow + 8 * piece) = ra[i];
+      *reinterpret_cast<u32x4_t*>(B + (prow + 32 * i) * kLdsRow + 8 * piece) = rb[i];
+    }
   };
-  load(a0, b0, 0);
-  int k = 0;
-  for (; k + 64 <= m; k += 64) {
-    load(a1, b1, k + 32);
-    mma(a0, b0);
-    if (k + 64 < m) load(a0, b0, k + 64);
-    mma(a1, b1);
+
+  floatx4_t acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  const int wm = (w >> 1) * 64, wn = (w & 1) * 64;   // this wave's 64 x 64 sub-tile
+
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  const int nst = m / kBK;
+  for (int st = 0; st < nst; ++st) {
+    const int buf = st & 1;
+    if (st + 1 < nst) gload((st + 1) * kBK);          // in flight while this stage multiplies
+    const bf16* A = lds + buf * kStageElems;
+    const bf16* B = A + kBM * kLdsRow;
+#pragma unroll
+    for (int ks = 0; ks < kBK / 32; ++ks) {
+      u32x4_t a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        a[i] = *reinterpret_cast<const u32x4_t*>(A + (wm + 16 * i + lr) * kLdsRow + 32 * ks + 8 * lq);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        b[j] = *reinterpret_cast<const u32x4_t*>(B + (wn + 16 * j + lr) * kLdsRow + 32 * ks + 8 * lq);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a[i]),
+                                                              __builtin_bit_cast(bf16x8_t, b[j]),
+                                                              acc[i][j], 0, 0, 0);
+    }
+    if (st + 1 < nst) lstore(buf ^ 1);
+    __syncthreads();
   }
-  if (k < m) mma(a0, b0);                       // m = 32 (mod 64): one step left
 
   // stores: lane holds tokens 4*lq + v of each token tile, column lr of each column tile
   const int64_t slot_end = num_pages * DCKV_PAGE_TOKENS;
 #pragma unroll
-  for (int i = 0; i < kAM; ++i) {
+  for (int i = 0; i < 4; ++i) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      const int t = tok_w + 16 * i + 4 * lq + v;
+      const int t = tok0 + wm + 16 * i + 4 * lq + v;
       if (t >= n_tok) continue;
       const int64_t sl = slot[t];
       if (sl < 0 || sl >= slot_end) continue;
       bf16* pg = pool + (sl / DCKV_PAGE_TOKENS) * page_elems;
       const int sp = int(sl % DCKV_PAGE_TOKENS);
 #pragma unroll
-      for (int j = 0; j < kAN; ++j) {
-        const int c = col_w + 16 * j + lr;
+      for (int j = 0; j < 4; ++j) {
+        const int c = col0 + wn + 16 * j + lr;
         if (c >= ncols) continue;
         const float val = acc[i][j][v];
         if (c < RK)
-          pg[int64_t(sp) * RKp + c] = static_cast<bf16>(val);
+          pg[key_elem(sp, c)] = static_cast<bf16>(val);
         else if (c < RKp)
-          pg[int64_t(sp) * RKp + c] = static_cast<bf16>(0.f);
+          pg[key_elem(sp, c)] = static_cast<bf16>(0.f);
         else
           pg[value_base + int64_t(c - RKp) * DCKV_PAGE_TOKENS + sp] = static_cast<bf16>(val);
       }
@@ -224,9 +255,9 @@ hipError_t launch_append(const dckv_plan& p, const void* x, int32_t n_tok, const
                          hipStream_t stream) {
   if (p.dtype == DCKV_F32)
     return launch_append_t<float>(p, x, n_tok, L_keys, L_value, slot, pool, num_pages, stream);
-  if (p.m % 32 == 0) {
+  if (p.m % kBK == 0) {
     const int ncols = p.RKp + p.rv;
-    dim3 grid((ncols + 127) / 128, (n_tok + 63) / 64);
+    dim3 grid((ncols + kBN - 1) / kBN, (n_tok + kBM - 1) / kBM);
     hipLaunchKernelGGL(append_mfma, grid, dim3(256), 0, stream, static_cast<const bf16*>(x),
                        static_cast<const bf16*>(L_keys), static_cast<const bf16*>(L_value), slot,
                        static_cast<bf16*>(pool), n_tok, p.m, p.RK, p.RKp, p.rv, p.page_elems,

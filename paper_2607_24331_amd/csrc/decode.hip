@@ -53,7 +53,7 @@ template <typename T>
 __global__ __launch_bounds__(kThreads) void split_valu(
     const float* __restrict__ qt, const T* __restrict__ pool, int64_t num_pages,
     const int32_t* __restrict__ page_table, int max_pages, const int32_t* __restrict__ seq_lens,
-    int max_context, int split_tokens, int n_split, int RKp, int rv, int64_t page_elems,
+    int max_context, int split_tokens, int n_split, int rv, int64_t page_elems,
     int64_t value_base, float* __restrict__ part_ml, float* __restrict__ part_acc, HeadTables tb) {
   const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x;
@@ -83,8 +83,12 @@ __global__ __launch_bounds__(kThreads) void split_valu(
     const T* pg = pool + (valid ? int64_t(page) * page_elems : 0);
     float sp = 0.f;
     if (valid && slot < n) {
-      const T* krow = pg + int64_t(slot) * RKp + koff;
-      for (int k = quarter; k < r; k += 4) sp = fmaf(qs[k], to_f32(krow[k]), sp);
+      // chunk-major keys: column c of this slot at (c/32)*2048 + slot*32 + c%32
+      const T* kslot = pg + slot * 32;
+      for (int k = quarter; k < r; k += 4) {
+        const int c = koff + k;
+        sp = fmaf(qs[k], to_f32(kslot[(c >> 5) * 2048 + (c & 31)]), sp);
+      }
     }
     part[quarter][slot] = sp;
     __syncthreads();
@@ -187,7 +191,7 @@ hipError_t launch_decode_t(const dckv_plan& p, const DecodeShape& sh, const floa
   if (p.prof_before && (e = hipEventRecord(p.prof_before, stream)) != hipSuccess) return e;
   hipLaunchKernelGGL(split_valu<T>, dim3(sh.n_split, p.Hq, sh.batch), dim3(kThreads), 0, stream, qt,
                      static_cast<const T*>(pool), num_pages, page_table, max_pages, seq_lens,
-                     sh.max_context, sh.split_tokens, sh.n_split, p.RKp, p.rv, p.page_elems,
+                     sh.max_context, sh.split_tokens, sh.n_split, p.rv, p.page_elems,
                      p.value_base, ml, acc, p.tables);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -220,14 +224,16 @@ DecodeShape decode_shape(const dckv_plan& p, int32_t batch, int32_t max_context)
   s.n_split = max_context > 0 ? int32_t((max_context + L - 1) / L) : 1;
   s.off_qt = 0;
   s.off_ml = align_up(size_t(batch) * p.qlen * sizeof(float), 256);
+  if (s.mfma)   // the MFMA path keeps hi/lo query blocks of 2 KB per (sequence, slice, chunk)
+    s.off_ml = align_up(size_t(batch) * p.mfma.n_slices * p.mfma.max_pairs * 2048, 256);
   if (s.mfma) {
     const int64_t units = int64_t(batch) * s.n_split;
     s.n_units = int32_t((units + 7) / 8 * 8);
     s.n_rchunks = mfma_merge_rank_chunks(p);
     const size_t nh = 16 * size_t(p.mfma.nt);
-    s.off_acc = s.off_ml;
-    const size_t part = size_t(batch) * p.mfma.n_slices * s.n_split * nh * (2 + size_t(p.rv));
-    s.off_opart = s.off_acc + align_up(part * sizeof(float), 256);
+    const size_t rows = size_t(batch) * p.mfma.n_slices * s.n_split;
+    s.off_acc = s.off_ml + align_up(rows * 2 * nh * sizeof(float), 256);
+    s.off_opart = s.off_acc + align_up(rows * nh * size_t(p.rv) * sizeof(float), 256);
     s.bytes = s.off_opart + align_up(size_t(batch) * p.Hq * p.rv * sizeof(float), 256);
   } else {
     const size_t rows = size_t(batch) * p.Hq * s.n_split;
@@ -242,16 +248,9 @@ hipError_t launch_decode(const dckv_plan& p, const DecodeShape& shape, const flo
                          const void* pool, int64_t num_pages, const int32_t* page_table,
                          int32_t max_pages, const int32_t* seq_lens, const void* R_keys,
                          const void* R_value, float* out, void* workspace, hipStream_t stream) {
-  if (shape.mfma) {
-    float* qt = reinterpret_cast<float*>(static_cast<char*>(workspace) + shape.off_qt);
-    const float scale = kLog2e / std::sqrt(float(p.dh));
-    hipLaunchKernelGGL(fold_kernel<bf16>, dim3(p.Hq, shape.batch), dim3(kThreads), 0, stream, q,
-                       static_cast<const bf16*>(R_keys), qt, p.tables, scale);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    return launch_decode_mfma(p, shape, qt, pool, num_pages, page_table, max_pages, seq_lens,
+  if (shape.mfma)
+    return launch_decode_mfma(p, shape, q, pool, num_pages, page_table, max_pages, seq_lens, R_keys,
                               R_value, out, workspace, stream);
-  }
   if (p.dtype == DCKV_F32)
     return launch_decode_t<float>(p, shape, q, pool, num_pages, page_table, max_pages, seq_lens,
                                   R_keys, R_value, out, workspace, stream);

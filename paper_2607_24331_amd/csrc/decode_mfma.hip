@@ -44,6 +44,7 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 // format, no swizzle); loads at or past num_records return zero.
 constexpr int kRsrcWord3 = 0x00020000;
 constexpr int kOutOfRange = 0x40000000;   // byte offset beyond any page
+constexpr int kNonTemporal = 2;           // cache policy of streamed latents: nt
 
 // One producer block: RING consecutive items of one page, all keys or all
 // values (kind 2: past the split, every load reads zero).
@@ -88,14 +89,74 @@ __device__ __forceinline__ float wave_sum16(float v) {
 }
 
 // ---------------------------------------------------------------------------
+// fold_blocks: the folded queries q~_h = q_h R_{g,h}^T * log2(e)/sqrt(d_h)
+// (Sec. III-A: q (z R)^T = (q R^T) z^T; Sec. III-C: head h meets only its
+// group's factor), written straight into the split kernel's B-operand blocks.
+// Block (slice, tile n, chunk c) holds, for head slot 16n + j and key column
+// 32c + kk, q~ of that slot's head at column kk - koff_g when the column lies
+// in the head's group latent, else zero; split as bf16 hi + lo parts.  B
+// operand order: lane 16*(kk/8) + j, element kk%8.  One wave per (block,
+// slot): 32 columns, two lanes a column (halves of d_h).
+__global__ __launch_bounds__(64) void fold_blocks(const float* __restrict__ q,
+                                                  const bf16* __restrict__ Rk,
+                                                  u32x4* __restrict__ qblk_ws, float scale,
+                                                  HeadTables tb, MfmaTables mt) {
+  const int pr = blockIdx.x, j = blockIdx.y;
+  const int J = mt.n_slices;
+  const int b = blockIdx.z / J, slice = blockIdx.z % J;
+  const int nch0 = mt.kc1[slice][0] - mt.kc0[slice][0];
+  const int npairs = nch0 + (mt.nt > 1 ? mt.kc1[slice][1] - mt.kc0[slice][1] : 0);
+  if (pr >= npairs) return;
+  const int n = pr < nch0 ? 0 : 1;
+  const int c = mt.kc0[slice][n] + pr - (n ? nch0 : 0);
+  const int h = mt.hord[slice][16 * n + j];
+  const int lane = threadIdx.x, kk = lane & 31, half = lane >> 5;
+  const int k = 32 * c + kk;
+  const int dh = tb.head_dim, hd = dh / 2, d0 = half * hd;   // d_h is a multiple of 8
+  float v = 0.f;
+  if (h >= 0) {
+    const int lo = tb.koff_of_q[h], r = tb.rank_of_q[h];
+    if (k >= lo && k < lo + r) {
+      const bf16* row = Rk + tb.roff_of_q[h] + int64_t(k - lo) * tb.rstride_of_q[h] + tb.rcol_of_q[h] + d0;
+      const float* qh = q + (int64_t(b) * tb.n_q_heads + h) * dh + d0;
+      // 8 columns a step: one 8-byte-aligned load of R (4 x bf16 pairs) and two float4 of q
+      for (int d = 0; d < hd; d += 8) {
+        uint32_t w4[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) w4[j] = *reinterpret_cast<const uint32_t*>(row + d + 2 * j);
+        const float4 qa = *reinterpret_cast<const float4*>(qh + d);
+        const float4 qb = *reinterpret_cast<const float4*>(qh + d + 4);
+        const float qv[8] = {qa.x, qa.y, qa.z, qa.w, qb.x, qb.y, qb.z, qb.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          v = fmaf(qv[2 * j], __uint_as_float(w4[j] << 16), v);
+          v = fmaf(qv[2 * j + 1], __uint_as_float(w4[j] & 0xFFFF0000u), v);
+        }
+      }
+    }
+  }
+  v += __shfl_xor(v, 32);
+  if (half == 0) {
+    v *= scale;
+    const bf16 vh = static_cast<bf16>(v);
+    const bf16 vl = static_cast<bf16>(v - static_cast<float>(vh));
+    bf16* blk = reinterpret_cast<bf16*>(qblk_ws + (int64_t(b * J + slice) * mt.max_pairs + pr) * 128);
+    const int l = 16 * (kk >> 3) + j, e = kk & 7;
+    blk[l * 8 + e] = vh;
+    blk[512 + l * 8 + e] = vl;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // W waves (4 or 8) a work-group; NT 16-head tiles; at most MTW value M-tiles
 // (16 ranks) a wave; RING loads in flight a wave.
 template <int W, int NT, int MTW, int RING>
 __global__ __launch_bounds__(W * 64, 1) void split_mfma(
-    const float* __restrict__ qt, const bf16* __restrict__ pool, int64_t num_pages,
+    const u32x4* __restrict__ qblk_ws, const bf16* __restrict__ pool, int64_t num_pages,
     const int32_t* __restrict__ page_table, int max_pages, const int32_t* __restrict__ seq_lens,
-    int max_context, int split_tokens, int n_split, int n_units, int RK, int RKp, int rv,
-    int64_t page_elems, int64_t value_base, float* __restrict__ part, HeadTables tb, MfmaTables mt) {
+    int max_context, int split_tokens, int n_split, int n_units, int RK, int rv,
+    int64_t page_elems, int64_t value_base, float* __restrict__ part_ml, float* __restrict__ part,
+    MfmaTables mt) {
   constexpr int NH = 16 * NT;                          // head slots of the slice
   constexpr int SW = (4 * NT < W) ? 4 * NT : W;        // waves holding score tiles
   constexpr int MPW = (4 * NT) / SW;                   // score M-tiles (16 tokens) a scoring wave
@@ -155,7 +216,7 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
   // lengths are whole blocks, so a producer block never spans two pages or
   // two kinds: its page and kind are set once per block, and each issue is a
   // single unconditional 16-byte buffer load (out-of-range offsets read 0).
-  const int lane_key = 2 * (lr * RKp + 8 * lq);       // byte offsets of this lane
+  const int lane_key = 2 * (lr * 32 + 8 * lq);        // byte offsets of this lane
   const int lane_val = 2 * (lr * 64 + 8 * lq);
   const int page_bytes = int(page_elems * 2);
   const int blocks_pp = (NK + NV) / RING;             // producer blocks a page
@@ -173,7 +234,9 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
     r.nval = page < np ? min(64, (t1 - t0) - page * 64) : 0;
     r.idx0 = blk * RING;                              // first item of the block
     r.kind = page >= np ? 2 : (r.idx0 < NK ? 0 : 1);
-    r.base = r.kind == 0 ? 2 * (16 * mb_w * RKp + 32 * (kc0_w + r.idx0 / MPW))
+    // key chunk c holds the 64 slots contiguously (2048 elements); M-tile m
+    // of it is the 512-element run starting at m * 512
+    r.base = r.kind == 0 ? 2 * (2048 * (kc0_w + r.idx0 / MPW) + 512 * mb_w)
                          : 2 * (int(value_base) + 16 * (mt0_w + (r.idx0 - NK) / 2) * 64);
     return r;
   };
@@ -183,7 +246,7 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
     if (pb.kind == 0) {
       const int i = pb.idx0 + s;
       const int c = kc0_w + i / MPW;
-      const int o = pb.base + 2 * (16 * (s % MPW) * RKp + 32 * (s / MPW)) + lane_key;
+      const int o = pb.base + 2 * (512 * (s % MPW) + 2048 * (s / MPW)) + lane_key;
       const bool ok = (i < nk_real) & (32 * c + 8 * lq < RK);     // no short-circuit branches
       off = ok ? o : kOutOfRange;
     } else if (pb.kind == 1) {
@@ -192,7 +255,7 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
       const bool ok = (mtl < mcnt_w) & (16 * (mt0_w + mtl) + lr < rv) & (32 * (s & 1) + 8 * lq < pb.nval);
       off = ok ? o : kOutOfRange;
     }
-    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(pb.rsrc, off, 0, 0));
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(pb.rsrc, off, 0, kNonTemporal));
   };
 
   u32x4 ring[RING];
@@ -202,41 +265,24 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
     for (int s = 0; s < RING; ++s) ring[s] = issue(pb0, s);
   }
 
-  // ---- block-diagonal folded query, hi/lo bf16, in MFMA B-operand order:
-  // block (tile n, chunk c), lane l, element e  <->  key column 32c + 8(l/16) + e,
-  // head slot 16n + l%16.
+  // ---- block-diagonal folded query (hi/lo bf16 MFMA B operands, built by
+  // fold_blocks): a straight 16-byte copy into LDS, eight loads in flight
+  // a thread, behind the ring's first loads.
   {
-    const float* qb = qt + int64_t(b) * tb.qlen;
-    for (int idx = tid; idx < npairs * 64; idx += W * 64) {
-      const int pr = idx >> 6, l = idx & 63;
-      const int n = (NT > 1 && pr >= nch0) ? 1 : 0;
-      const int c = mt.kc0[slice][n] + pr - (n ? nch0 : 0);
-      const int h = mt.hord[slice][16 * n + (l & 15)];
-      int lo = 0, cnt = 0, qo = 0;
-      if (h >= 0) {
-        lo = tb.koff_of_q[h];
-        cnt = tb.rank_of_q[h];
-        qo = tb.qoff[h];
-      }
-      uint32_t hi_w[4], lo_w[4];
+    const u32x4* src = qblk_ws + int64_t(b * J + slice) * mt.max_pairs * 128;
+    const int n16 = npairs * 128;
+    for (int base = tid; base < n16; base += 8 * W * 64) {
+      u32x4 v[8];
 #pragma unroll
-      for (int e2 = 0; e2 < 4; ++e2) {
-        uint32_t hw = 0, lw = 0;
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-          const int k = 32 * c + 8 * (l >> 4) + 2 * e2 + half;
-          float v = 0.f;
-          if (k >= lo && k < lo + cnt) v = qb[qo + k - lo];
-          const bf16 vh = static_cast<bf16>(v);
-          const bf16 vl = static_cast<bf16>(v - static_cast<float>(vh));
-          hw |= uint32_t(__builtin_bit_cast(uint16_t, vh)) << (16 * half);
-          lw |= uint32_t(__builtin_bit_cast(uint16_t, vl)) << (16 * half);
-        }
-        hi_w[e2] = hw;
-        lo_w[e2] = lw;
+      for (int k = 0; k < 8; ++k) {
+        const int idx = base + k * W * 64;
+        if (idx < n16) v[k] = src[idx];
       }
-      qblk[(pr * 2 + 0) * 64 + l] = u32x4{hi_w[0], hi_w[1], hi_w[2], hi_w[3]};
-      qblk[(pr * 2 + 1) * 64 + l] = u32x4{lo_w[0], lo_w[1], lo_w[2], lo_w[3]};
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int idx = base + k * W * 64;
+        if (idx < n16) qblk[idx] = v[k];
+      }
     }
   }
   __syncthreads();
@@ -382,16 +428,17 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
     }
   }
 
-  // ---- partials: m[NH], l[NH], acc[rank][NH] (head slot fastest)
-  float* pb = part + ((int64_t(b) * J + slice) * n_split + split) * int64_t(NH * (2 + rv));
+  // ---- partials: (m[NH], l[NH]) compact per split, acc[rank][NH] (head slot fastest)
+  const int64_t prow = (int64_t(b) * J + slice) * n_split + split;
   if (w == 0 && lane < 16) {
+    float* pml = part_ml + prow * (2 * NH);
 #pragma unroll
     for (int n = 0; n < NT; ++n) {
-      pb[16 * n + lane] = m_run[n];
-      pb[NH + 16 * n + lane] = l_run[n];
+      pml[16 * n + lane] = m_run[n];
+      pml[NH + 16 * n + lane] = l_run[n];
     }
   }
-  float* pa = pb + 2 * NH;
+  float* pa = part + prow * int64_t(NH) * rv;
 #pragma unroll
   for (int i = 0; i < MTW; ++i) {
     if (i < mcnt_w) {
@@ -409,20 +456,24 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
 
 // ---------------------------------------------------------------------------
 // Merge: a[b][h][r] = sum_s 2^(m_s - M) acc_s[r] / sum_s 2^(m_s - M) l_s.
-// Grid (value-rank chunks of kMergeRanks, batch * slices), 256 threads.  A
-// split row of the chunk is kMergeRanks * NH contiguous floats; TPR threads
-// cover it with float4 loads (4 head slots each) and the 256 / TPR thread
-// groups take the splits round-robin.  Fixed order: group g sums splits
-// g, g + G, ... in ascending order, then the G group sums are added in order.
+// Grid (value-rank chunks of kMergeRanks, batch * slices), 256 threads.
+// Pass 1: per head slot the maximum M and the weighted sum L over splits,
+// read from the compact (m, l) rows, eight independent loads a thread.
+// Pass 2: a split row of the chunk is kMergeRanks * NH contiguous floats;
+// TPR threads cover it with float4 loads (4 head slots each) and the
+// 256 / TPR thread groups take the splits round-robin, four splits in flight.
+// Fixed order: group g sums splits g, g + G, ... ascending, then the G group
+// sums are added in order.
 template <int NH>
-__global__ __launch_bounds__(256) void merge_mfma(const float* __restrict__ part,
+__global__ __launch_bounds__(256) void merge_mfma(const float* __restrict__ part_ml,
+                                                  const float* __restrict__ part,
                                                   const int32_t* __restrict__ seq_lens,
                                                   int max_context, int split_tokens, int n_split,
                                                   int rv, float* __restrict__ amerged,
                                                   HeadTables tb, MfmaTables mt) {
   constexpr int TPR = kMergeRanks * NH / 4;   // threads a split row
   constexpr int G = 256 / TPR;                // split groups
-  constexpr int SUB = 256 / NH;               // split groups of the max / sum pass
+  constexpr int SUB = 256 / NH;               // split groups of pass 1
   const int rc = blockIdx.x;
   const int bj = blockIdx.y;
   const int J = mt.n_slices;
@@ -434,14 +485,22 @@ __global__ __launch_bounds__(256) void merge_mfma(const float* __restrict__ part
   int T_b = seq_lens[b];
   T_b = T_b < 0 ? 0 : (T_b > max_context ? max_context : T_b);
   const int ns = (T_b + split_tokens - 1) / split_tokens;
-  const int64_t stride = int64_t(NH) * (2 + rv);
-  const float* pb = part + (int64_t(b) * J + slice) * n_split * stride;
+  const float* ml = part_ml + (int64_t(b) * J + slice) * n_split * (2 * NH);
+  const float* pb = part + (int64_t(b) * J + slice) * n_split * int64_t(NH) * rv;
 
-  // pass 1: per head slot maximum, then the weighted sum of l
+  // pass 1
   {
     const int h = tid % NH, sub = tid / NH;
     float mx = -INFINITY;
-    for (int s = sub; s < ns; s += SUB) mx = fmaxf(mx, pb[s * stride + h]);
+    int s = sub;
+    for (; s + 7 * SUB < ns; s += 8 * SUB) {
+      float v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) v[k] = ml[(s + k * SUB) * (2 * NH) + h];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) mx = fmaxf(mx, v[k]);
+    }
+    for (; s < ns; s += SUB) mx = fmaxf(mx, ml[s * (2 * NH) + h]);
     red[tid] = mx;
     __syncthreads();
     if (tid < NH) {
@@ -452,8 +511,20 @@ __global__ __launch_bounds__(256) void merge_mfma(const float* __restrict__ part
     __syncthreads();
     const float M = sM[h];
     float l = 0.f;
-    if (M != -INFINITY)
-      for (int s = sub; s < ns; s += SUB) l += exp2f(pb[s * stride + h] - M) * pb[s * stride + NH + h];
+    if (M != -INFINITY) {
+      s = sub;
+      for (; s + 7 * SUB < ns; s += 8 * SUB) {
+        float mv[8], lv[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          mv[k] = ml[(s + k * SUB) * (2 * NH) + h];
+          lv[k] = ml[(s + k * SUB) * (2 * NH) + NH + h];
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) l += exp2f(mv[k] - M) * lv[k];
+      }
+      for (; s < ns; s += SUB) l += exp2f(ml[s * (2 * NH) + h] - M) * ml[s * (2 * NH) + NH + h];
+    }
     red[tid] = l;
     __syncthreads();
     if (tid < NH) {
@@ -464,7 +535,7 @@ __global__ __launch_bounds__(256) void merge_mfma(const float* __restrict__ part
     __syncthreads();
   }
 
-  // pass 2: weighted sum of the chunk's accumulators
+  // pass 2
   const int g = tid / TPR, e = tid % TPR;
   const int rl = e / (NH / 4);                 // rank inside the chunk
   const int hq = (e % (NH / 4)) * 4;           // first of four head slots
@@ -472,13 +543,14 @@ __global__ __launch_bounds__(256) void merge_mfma(const float* __restrict__ part
   const float4 M4 = make_float4(sM[hq], sM[hq + 1], sM[hq + 2], sM[hq + 3]);
   float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
   if (r < rv) {
-    const float* src = pb + 2 * NH + int64_t(r) * NH + hq;
+    const float* src = pb + int64_t(r) * NH + hq;
+    const int64_t stride = int64_t(NH) * rv;
     int s = g;
     for (; s + 3 * G < ns; s += 4 * G) {
       float4 mv[4], av[4];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        mv[k] = *reinterpret_cast<const float4*>(pb + (s + k * G) * stride + hq);
+        mv[k] = *reinterpret_cast<const float4*>(ml + (s + k * G) * (2 * NH) + hq);
         av[k] = *reinterpret_cast<const float4*>(src + (s + k * G) * stride);
       }
 #pragma unroll
@@ -490,7 +562,7 @@ __global__ __launch_bounds__(256) void merge_mfma(const float* __restrict__ part
       }
     }
     for (; s < ns; s += G) {
-      const float4 mv = *reinterpret_cast<const float4*>(pb + s * stride + hq);
+      const float4 mv = *reinterpret_cast<const float4*>(ml + s * (2 * NH) + hq);
       const float4 av = *reinterpret_cast<const float4*>(src + s * stride);
       a.x = fmaf(exp2f(mv.x - M4.x), av.x, a.x);
       a.y = fmaf(exp2f(mv.y - M4.y), av.y, a.y);
@@ -539,8 +611,7 @@ __global__ __launch_bounds__(256) void upproj(const float* __restrict__ amerged,
   const int row0 = rbk * RB;
   const int nrow = min(RB, rows - row0);
   if (nrow <= 0) return;
-  extern __shared__ float sa[];                // [RB][rv]
-  __shared__ float red[64][33];
+  extern __shared__ float sa[];                // [RB][rv], then [64][RB][32] partial sums
   for (int i = tid; i < nrow * rv; i += 256) {
     const int q = i / rv, r = i - q * rv;
     const int row = row0 + q;
@@ -583,56 +654,57 @@ __global__ __launch_bounds__(256) void upproj(const float* __restrict__ amerged,
     }
     for (; r < rv; r += 64) fma8(load16(src + int64_t(r) * n), r);
   }
+  // one reduction round: every thread's 8 rows x 8 columns go to LDS, then
+  // each of the 256 outputs sums its 64 rank groups in order
+  float* red = sa + RB * rv;                   // [64 rank groups][RB rows][32 columns]
+  __syncthreads();
 #pragma unroll
-  for (int q = 0; q < RB; ++q) {
-    if (q >= nrow) break;                      // block-uniform
+  for (int q = 0; q < RB; ++q)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) red[rg][8 * c8 + j] = acc[q][j];
-    __syncthreads();
-    if (tid < 32) {
-      float t = red[0][tid];
-      for (int k = 1; k < 64; ++k) t += red[k][tid];
-      const int cc = ct * 32 + tid;
-      if (cc < dh) {
-        const int row = row0 + q;
-        const int b = row / qpk, h = kv * qpk + row % qpk;
-        out[(int64_t(b) * tb.n_q_heads + h) * dh + cc] = t;
-      }
+    for (int j = 0; j < 8; ++j) red[(rg * RB + q) * 32 + 8 * c8 + j] = acc[q][j];
+  __syncthreads();
+  {
+    const int q = tid / 32, cc = tid % 32;
+    if (q < nrow && ct * 32 + cc < dh) {
+      float t = 0.f;
+      for (int k = 0; k < 64; ++k) t += red[(k * RB + q) * 32 + cc];
+      const int row = row0 + q;
+      const int b = row / qpk, h = kv * qpk + row % qpk;
+      out[(int64_t(b) * tb.n_q_heads + h) * dh + ct * 32 + cc] = t;
     }
-    __syncthreads();
   }
 }
 
 template <int W, int NT, int MTW>
-hipError_t launch_split(const dckv_plan& p, const DecodeShape& sh, const float* qt,
+hipError_t launch_split(const dckv_plan& p, const DecodeShape& sh, const u32x4* qblk,
                         const void* pool, int64_t num_pages, const int32_t* page_table,
-                        int32_t max_pages, const int32_t* seq_lens, float* part,
+                        int32_t max_pages, const int32_t* seq_lens, float* part_ml, float* part,
                         size_t lds, hipStream_t stream) {
-  constexpr int RING = (W == 4) ? 16 : 8;
+  constexpr int RING = 16;
   auto kern = split_mfma<W, NT, MTW, RING>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
   if (e != hipSuccess) return e;
   const int grid = sh.n_units * p.mfma.n_slices;
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(W * 64), lds, stream, qt,
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(W * 64), lds, stream, qblk,
                      static_cast<const bf16*>(pool), num_pages, page_table, max_pages, seq_lens,
-                     sh.max_context, sh.split_tokens, sh.n_split, sh.batch * sh.n_split, p.RK, p.RKp, p.rv,
-                     p.page_elems, p.value_base, part, p.tables, p.mfma);
+                     sh.max_context, sh.split_tokens, sh.n_split, sh.batch * sh.n_split, p.RK,
+                     p.rv, p.page_elems, p.value_base, part_ml, part, p.mfma);
   return hipGetLastError();
 }
 
 template <int W, int NT>
-hipError_t launch_split_w(const dckv_plan& p, const DecodeShape& sh, const float* qt,
+hipError_t launch_split_w(const dckv_plan& p, const DecodeShape& sh, const u32x4* qt,
                           const void* pool, int64_t num_pages, const int32_t* page_table,
-                          int32_t max_pages, const int32_t* seq_lens, float* part, size_t lds,
-                          hipStream_t stream) {
+                          int32_t max_pages, const int32_t* seq_lens, float* part_ml, float* part,
+                          size_t lds, hipStream_t stream) {
   const int mtw = p.mfma.mtw;
   if (mtw <= 8)
-    return launch_split<W, NT, 8>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part, lds, stream);
+    return launch_split<W, NT, 8>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, lds, stream);
   if (mtw <= 16)
-    return launch_split<W, NT, 16>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part, lds, stream);
+    return launch_split<W, NT, 16>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, lds, stream);
   if (NT == 1 && mtw <= 32)
-    return launch_split<W, NT, (NT == 1 ? 32 : 16)>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part, lds, stream);
+    return launch_split<W, NT, (NT == 1 ? 32 : 16)>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, lds, stream);
   return hipErrorInvalidValue;
 }
 
@@ -646,37 +718,43 @@ int mfma_merge_rank_chunks(const dckv_plan& p) { return (p.rv + kMergeRanks - 1)
 
 int mfma_max_split_tokens() { return kPageSlots * DCKV_PAGE_TOKENS; }
 
-hipError_t launch_decode_mfma(const dckv_plan& p, const DecodeShape& sh, const float* qt,
+hipError_t launch_decode_mfma(const dckv_plan& p, const DecodeShape& sh, const float* q,
                               const void* pool, int64_t num_pages, const int32_t* page_table,
-                              int32_t max_pages, const int32_t* seq_lens, const void* R_value,
-                              float* out, void* workspace, hipStream_t stream) {
+                              int32_t max_pages, const int32_t* seq_lens, const void* R_keys,
+                              const void* R_value, float* out, void* workspace, hipStream_t stream) {
   char* ws = static_cast<char*>(workspace);
+  u32x4* qt = reinterpret_cast<u32x4*>(ws + sh.off_qt);
+  float* part_ml = reinterpret_cast<float*>(ws + sh.off_ml);
   float* part = reinterpret_cast<float*>(ws + sh.off_acc);
   float* amerged = reinterpret_cast<float*>(ws + sh.off_opart);
   const size_t lds = mfma_split_lds_bytes(p);
-  hipError_t e;
+  const float scale = kLog2e / std::sqrt(float(p.dh));
+  hipLaunchKernelGGL(fold_blocks, dim3(p.mfma.max_pairs, 16, sh.batch * p.mfma.n_slices), dim3(64),
+                     0, stream, q, static_cast<const bf16*>(R_keys), qt, scale, p.tables, p.mfma);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   if (p.prof_before && (e = hipEventRecord(p.prof_before, stream)) != hipSuccess) return e;
   if (p.mfma.waves == 4)
     e = p.mfma.nt == 1
-            ? launch_split_w<4, 1>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part, lds, stream)
-            : launch_split_w<4, 2>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part, lds, stream);
+            ? launch_split_w<4, 1>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, lds, stream)
+            : launch_split_w<4, 2>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, lds, stream);
   else
     e = p.mfma.nt == 1
-            ? launch_split_w<8, 1>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part, lds, stream)
-            : launch_split_w<8, 2>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part, lds, stream);
+            ? launch_split_w<8, 1>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, lds, stream)
+            : launch_split_w<8, 2>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, lds, stream);
   if (e != hipSuccess) return e;
   if (p.prof_after && (e = hipEventRecord(p.prof_after, stream)) != hipSuccess) return e;
   if (p.mfma.nt == 1)
     hipLaunchKernelGGL(merge_mfma<16>, dim3(sh.n_rchunks, sh.batch * p.mfma.n_slices), dim3(256), 0,
-                       stream, part, seq_lens, sh.max_context, sh.split_tokens, sh.n_split, p.rv,
-                       amerged, p.tables, p.mfma);
+                       stream, part_ml, part, seq_lens, sh.max_context, sh.split_tokens,
+                       sh.n_split, p.rv, amerged, p.tables, p.mfma);
   else
     hipLaunchKernelGGL(merge_mfma<32>, dim3(sh.n_rchunks, sh.batch * p.mfma.n_slices), dim3(256), 0,
-                       stream, part, seq_lens, sh.max_context, sh.split_tokens, sh.n_split, p.rv,
-                       amerged, p.tables, p.mfma);
+                       stream, part_ml, part, seq_lens, sh.max_context, sh.split_tokens,
+                       sh.n_split, p.rv, amerged, p.tables, p.mfma);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int rows = sh.batch * p.qpk;
-  const size_t lds_up = size_t(8) * p.rv * sizeof(float);
+  const size_t lds_up = (size_t(8) * p.rv + 64 * 8 * 32) * sizeof(float);
   e = hipFuncSetAttribute(reinterpret_cast<const void*>(upproj),
                           hipFuncAttributeMaxDynamicSharedMemorySize, int(lds_up));
   if (e != hipSuccess) return e;

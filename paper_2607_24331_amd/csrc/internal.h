@@ -67,7 +67,7 @@ struct DecodeShape {
 }  // namespace dckv
 
 struct dckv_plan {
-  int32_t m, Hq, Hkv, dh, G, rv, dtype, split_tokens, head_slices;
+  int32_t m, Hq, Hkv, dh, G, rv, dtype, split_tokens, head_slices, decode_waves;
   int32_t RK, RKp, qpk, qlen;
   int64_t page_elems, value_base, key_factor_elems;
   std::vector<int32_t> group_of_kv, ranks, hg, pos_in_group, koff, qoff;
@@ -88,10 +88,10 @@ void build_mfma_tables(dckv_plan& p);
 size_t mfma_split_lds_bytes(const dckv_plan& p);
 int mfma_merge_rank_chunks(const dckv_plan& p);
 int mfma_max_split_tokens();
-hipError_t launch_decode_mfma(const dckv_plan& p, const DecodeShape& sh, const float* qt,
+hipError_t launch_decode_mfma(const dckv_plan& p, const DecodeShape& sh, const float* q,
                               const void* pool, int64_t num_pages, const int32_t* page_table,
-                              int32_t max_pages, const int32_t* seq_lens, const void* R_value,
-                              float* out, void* workspace, hipStream_t stream);
+                              int32_t max_pages, const int32_t* seq_lens, const void* R_keys,
+                              const void* R_value, float* out, void* workspace, hipStream_t stream);
 
 // Defined in the kernel sources.
 DecodeShape decode_shape(const dckv_plan& p, int32_t batch, int32_t max_context);

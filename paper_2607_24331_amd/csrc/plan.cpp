@@ -79,7 +79,7 @@ void build_mfma_tables(dckv_plan& p) {
   t.mt_v = (p.rv + 15) / 16;
   // Accumulators take nt * mtw * 4 registers a lane: four waves while that
   // stays within 128, else eight waves (two a SIMD) with half the ranks each.
-  t.waves = (t.nt * ((t.mt_v + 3) / 4) <= 32) ? 4 : 8;
+  t.waves = p.decode_waves ? p.decode_waves : ((t.nt * ((t.mt_v + 3) / 4) <= 32) ? 4 : 8);
   t.mtw = (t.mt_v + t.waves - 1) / t.waves;
   if (t.nt * t.mtw > 32) return;               // beyond 128 accumulator registers a lane
   const int64_t lds = int64_t(max_pairs) * 2048 + 32 * 72 * 2 + 2 * 8 * 32 * 4 + 256 * 4;
@@ -116,6 +116,8 @@ int dckv_plan_create(const dckv_layer_desc* d, dckv_plan** out) {
   if (d->split_tokens < 0 || d->split_tokens % DCKV_PAGE_TOKENS != 0 || d->split_tokens > (1 << 24))
     return fail(DCKV_EINVAL, "plan_create: split_tokens %d is not 0 or a positive multiple of %d",
                 d->split_tokens, DCKV_PAGE_TOKENS);
+  if (d->decode_waves != 0 && d->decode_waves != 4 && d->decode_waves != 8)
+    return fail(DCKV_EINVAL, "plan_create: decode_waves %d is not 0, 4 or 8", d->decode_waves);
   if (d->head_slices < 0 || d->head_slices > DCKV_MAX_HEADS)
     return fail(DCKV_EINVAL, "plan_create: head_slices %d outside [0,%d]", d->head_slices,
                 DCKV_MAX_HEADS);
@@ -153,6 +155,7 @@ int dckv_plan_create(const dckv_layer_desc* d, dckv_plan** out) {
     p->dtype = d->latent_dtype;
     p->split_tokens = d->split_tokens;
     p->head_slices = d->head_slices;
+    p->decode_waves = d->decode_waves;
     p->group_of_kv.assign(d->group_of_kv_head, d->group_of_kv_head + Hkv);
     p->ranks.assign(d->group_rank, d->group_rank + G);
     p->hg = hg;
@@ -169,7 +172,7 @@ int dckv_plan_create(const dckv_layer_desc* d, dckv_plan** out) {
     }
     p->roff[G] = racc;
     p->RK = acc;
-    p->RKp = (acc + 7) / 8 * 8;
+    p->RKp = (acc + 31) / 32 * 32;              // whole 32-column key chunks
     p->key_factor_elems = racc;
     p->page_elems = int64_t(DCKV_PAGE_TOKENS) * p->RKp + int64_t(DCKV_PAGE_TOKENS) * p->rv;
     p->value_base = int64_t(DCKV_PAGE_TOKENS) * p->RKp;
@@ -223,13 +226,14 @@ int dckv_plan_info(const dckv_plan* p, dckv_plan_geometry* geo, int32_t* koff,
   if (!p) return fail(DCKV_EINVAL, "plan_info: null plan");
   if (geo) {
     geo->key_rank_total = p->RK;
-    geo->key_row_stride = p->RKp;
+    geo->key_width_padded = p->RKp;
     geo->value_rank = p->rv;
     geo->q_per_kv = p->qpk;
     geo->folded_query_len = p->qlen;
     geo->split_tokens = p->split_tokens;
     geo->mfma_path = p->mfma_ok ? 1 : 0;
     geo->head_slices = p->mfma_ok ? p->mfma.n_slices : 0;
+    geo->decode_waves = p->mfma_ok ? p->mfma.waves : 0;
     geo->page_elems = p->page_elems;
     geo->value_base = p->value_base;
     geo->key_factor_elems = p->key_factor_elems;

@@ -42,7 +42,8 @@ class Plan:
 
     def __init__(self, hidden: int, num_q_heads: int, num_kv_heads: int, head_dim: int,
                  group_of_kv_head: Sequence[int], group_rank: Sequence[int], value_rank: int,
-                 dtype: str = "bf16", split_tokens: int = 0, head_slices: int = 0):
+                 dtype: str = "bf16", split_tokens: int = 0, head_slices: int = 0,
+                 decode_waves: int = 0):
         if dtype not in _DTYPES:
             raise ValueError(f"dtype must be one of {sorted(_DTYPES)}")
         self.dtype = dtype
@@ -52,7 +53,8 @@ class Plan:
         desc = capi.LayerDesc(hidden, num_q_heads, num_kv_heads, head_dim, len(group_rank),
                               ctypes.cast(self._gmap, ctypes.POINTER(ctypes.c_int32)),
                               ctypes.cast(self._ranks, ctypes.POINTER(ctypes.c_int32)),
-                              value_rank, _DTYPES[dtype][0], split_tokens, head_slices)
+                              value_rank, _DTYPES[dtype][0], split_tokens, head_slices,
+                              decode_waves)
         handle = ctypes.c_void_p()
         _check(_lib.dckv_plan_create(ctypes.byref(desc), ctypes.byref(handle)), "plan_create")
         self._handle = handle
@@ -61,7 +63,7 @@ class Plan:
         info = self.info()
         self.geometry = info["geometry"]
         self.key_rank_total = self.geometry["key_rank_total"]
-        self.key_row_stride = self.geometry["key_row_stride"]
+        self.key_width_padded = self.geometry["key_width_padded"]
         self.page_elems = self.geometry["page_elems"]
         self.split_tokens = self.geometry["split_tokens"]
         self.key_factor_elems = self.geometry["key_factor_elems"]

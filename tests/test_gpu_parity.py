@@ -202,10 +202,10 @@ def test_append_layout_bit_exact_on_exact_inputs():
     sentinel = np.float32(-7.0)
     ref = np.full((pages, olayout.page_elems(wl.key_rank_total, wl.value_rank)), sentinel, np.float32)
     oappend.append(ref, table, 0, start, x, Lk, Lv, "bf16")
-    # the oracle's packing writes the padding columns of written rows as zero
-    RK, RKp = wl.key_rank_total, olayout.key_row_stride(wl.key_rank_total)
+    # the padding key columns of written slots are zero
+    RK, RKp = wl.key_rank_total, olayout.key_width_padded(wl.key_rank_total)
     for p in pos:
-        ref[table[0, p // 64], (p % 64) * RKp + RK:(p % 64) * RKp + RKp] = 0
+        ref[table[0, p // 64], olayout.key_offset(p % 64, np.arange(RK, RKp), RK)] = 0
     plan = plan_for(wl, split)
     from paper_2607_24331_amd import latent_append
     pool = dev(np.full(ref.shape, sentinel, np.float32), "bf16")

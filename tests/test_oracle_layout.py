@@ -8,8 +8,8 @@ from oracle import layout
 
 @pytest.mark.parametrize("RK, rv", [(1, 1), (7, 3), (8, 8), (43, 17), (128, 128), (1228, 1536)])
 def test_offsets_are_a_bijection_onto_the_page(RK, rv):
-    RKp = layout.key_row_stride(RK)
-    assert RKp % 8 == 0 and RK <= RKp < RK + 8
+    RKp = layout.key_width_padded(RK)
+    assert RKp % 32 == 0 and RK <= RKp < RK + 32
     n = layout.page_elems(RK, rv)
     used = np.zeros(n, dtype=np.int64)
     s = np.arange(64)[:, None]
@@ -18,21 +18,29 @@ def test_offsets_are_a_bijection_onto_the_page(RK, rv):
     np.add.at(used, used_k, 1)
     np.add.at(used, used_v, 1)
     # every latent element has its own slot; the only unused slots are the
-    # key-row padding columns RK..RKp-1
+    # key padding columns RK..RKp-1 of every token
     assert used.max() == 1
     pad = np.flatnonzero(used == 0)
-    expect_pad = (np.arange(64)[:, None] * RKp + np.arange(RK, RKp)[None, :]).ravel()
+    expect_pad = layout.key_offset(s, np.arange(RK, RKp)[None, :], RK).ravel()
     assert np.array_equal(np.sort(pad), np.sort(expect_pad))
 
 
 def test_hand_offsets():
-    # R_K = 10 -> rows of 16; r_v = 3
-    assert layout.key_row_stride(10) == 16
-    assert layout.page_elems(10, 3) == 64 * 16 + 64 * 3
-    assert layout.key_offset(0, 0, 10) == 0
-    assert layout.key_offset(2, 9, 10) == 2 * 16 + 9
-    assert layout.value_offset(0, 0, 10) == 1024
-    assert layout.value_offset(5, 2, 10) == 1024 + 2 * 64 + 5
+    # R_K = 40 -> two chunks of 32 (64 padded columns); r_v = 3
+    assert layout.key_width_padded(40) == 64
+    assert layout.page_elems(40, 3) == 64 * 64 + 64 * 3
+    assert layout.key_offset(0, 0, 40) == 0
+    assert layout.key_offset(0, 31, 40) == 31
+    assert layout.key_offset(1, 0, 40) == 32           # next slot, same chunk
+    assert layout.key_offset(2, 33, 40) == 2048 + 2 * 32 + 1   # second chunk
+    assert layout.value_offset(0, 0, 40) == 4096
+    assert layout.value_offset(5, 2, 40) == 4096 + 2 * 64 + 5
+
+
+def test_mfma_tile_is_contiguous():
+    # 16 consecutive slots x one 32-column chunk occupy 1 KB of bf16 in one run
+    offs = layout.key_offset(np.arange(16, 32)[:, None], np.arange(64, 96)[None, :], 100)
+    assert np.array_equal(np.sort(offs.ravel()), np.arange(offs.min(), offs.min() + 512))
 
 
 def test_pack_unpack_through_permuted_pages():
