@@ -106,6 +106,46 @@ def algorithmic_bytes(wl):
                 decode_total=latent + factors + qo)
 
 
+KERNEL_SOURCES = ("paper_2607_24331_amd/csrc/decode_mfma.hip", "paper_2607_24331_amd/csrc/plan.cpp",
+                  "paper_2607_24331_amd/csrc/internal.h")
+
+
+def kernel_sources_sha256():
+    import hashlib
+    h = hashlib.sha256()
+    root = os.path.dirname(os.path.abspath(__file__))
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(root, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(wl, launch):
+    """HBM bytes per launch of the split kernel from the committed counter
+    summary (FETCH_SIZE and WRITE_SIZE, each scaled by the same counter's
+    reading for a plain device copy of known size), or None when there is
+    no summary for this workload and launch shape, or the kernel sources
+    changed since the counters were taken."""
+    root = os.path.dirname(os.path.abspath(__file__))
+    path = os.path.join(root, "profiles", f"split_mfma_{wl.name}_counters.md")
+    if not os.path.exists(path):
+        return None
+    keys = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and line.split(":", 1)[0].strip() in (
+                    "workload", "launch", "kernel_sources_sha256", "traffic_bytes_per_launch"):
+                k, v = line.split(":", 1)
+                keys[k.strip()] = v.strip()
+    if (keys.get("workload") != wl.name or keys.get("launch") != launch
+            or keys.get("kernel_sources_sha256") != kernel_sources_sha256()):
+        return None
+    try:
+        return int(keys["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(wl, budget_s):
     """The oracle, as it stands, on a bounded sample of the same workload:
     the append of all new tokens plus whole-context decode of as many heads
@@ -221,6 +261,9 @@ def main():
           file=sys.stderr, flush=True)
 
     nb = algorithmic_bytes(wl)
+    launch = (f"split_tokens={split_used} head_slices={plan.geometry['head_slices']} "
+              f"decode_waves={plan.geometry['decode_waves']}")
+    traffic = measured_traffic(wl, launch) if mfma else None
     achieved = nb["latent"] / (kern_ms * 1e-3) / 1e9
     value = wl.batch / (ms_step * 1e-3)
     rec = {
@@ -257,9 +300,10 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
-            "traffic": None,
+            "traffic": traffic,
             "kernel_ms": kern_ms,
             "bytes_per_launch": nb["latent"],
+            "launch": launch,
         },
     }
     if not args.no_cpu_baseline:

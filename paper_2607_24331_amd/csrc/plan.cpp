@@ -77,9 +77,10 @@ void build_mfma_tables(dckv_plan& p) {
   }
   t.max_pairs = max_pairs;
   t.mt_v = (p.rv + 15) / 16;
-  // Accumulators take nt * mtw * 4 registers a lane: four waves while that
-  // stays within 128, else eight waves (two a SIMD) with half the ranks each.
-  t.waves = p.decode_waves ? p.decode_waves : ((t.nt * ((t.mt_v + 3) / 4) <= 32) ? 4 : 8);
+  // Eight waves (two a SIMD, so one wave's loads overlap the other's MFMAs)
+  // whenever every wave gets at least one 16-rank value tile; four waves
+  // for very small value ranks.  Accumulators take nt * mtw * 4 registers.
+  t.waves = p.decode_waves ? p.decode_waves : (t.mt_v >= 8 ? 8 : 4);
   t.mtw = (t.mt_v + t.waves - 1) / t.waves;
   if (t.nt * t.mtw > 32) return;               // beyond 128 accumulator registers a lane
   const int64_t lds = int64_t(max_pairs) * 2048 + 32 * 72 * 2 + 2 * 8 * 32 * 4 + 256 * 4;
