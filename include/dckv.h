@@ -98,8 +98,9 @@ typedef struct dckv_layer_desc {
                                       work-groups (bf16 path); 0 for the default
                                       (one slice per 32 heads) */
   int32_t decode_waves;            /* waves of a bf16 decode work-group: 4 or 8,
-                                      or 0 for the default (fewest that keep the
-                                      accumulators within 128 registers a lane) */
+                                      or 0 for the default (eight when every wave
+                                      gets at least one 16-rank value tile, i.e.
+                                      r_v > 112, else four) */
 } dckv_layer_desc;
 
 /* Derived layout facts of a plan. */
