@@ -32,6 +32,11 @@ HIPCC_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
 ]
+# Per-source extras.  The append GEMM keeps its MFMA accumulators in
+# ordinary VGPRs: with the default AGPR form the register allocator rotated
+# accumulators through AGPR copies inside the k loop, each copy waiting for
+# an in-flight MFMA.
+HIPCC_EXTRA = {"append.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-D__HIP_PLATFORM_AMD__", "-Wall", "-Wextra"]
 
 
@@ -58,8 +63,8 @@ def build(verbose: bool = False) -> str:
         objs.append(obj)
     for src in HIP_SOURCES:
         obj = os.path.join(BUILD, src + ".o")
-        _run([hipcc, *HIPCC_FLAGS, "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, src),
-              "-o", obj], verbose)
+        _run([hipcc, *HIPCC_FLAGS, *HIPCC_EXTRA.get(src, []), "-I", INCLUDE, "-I", CSRC, "-c",
+              os.path.join(CSRC, src), "-o", obj], verbose)
         objs.append(obj)
     tmp = LIB + ".tmp"
     _run([hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, *objs], verbose)

@@ -102,47 +102,81 @@ __global__ __launch_bounds__(256) void append_valu(const T* __restrict__ x, cons
 
 // bf16 MFMA kernel (m a multiple of 64).  Output C[token][column] =
 // sum_k x[token][k] * LT[column][k]: both operands are contiguous in k.
-// Work-group tile 128 tokens x 128 columns, four waves of 64 x 64 (4 x 4
-// tiles of 16 x 16); k advances in stages of 64 staged through LDS (rows
-// padded to 72 elements so the 16 rows an MFMA operand load touches fall in
-// distinct banks), two stages in flight: the next stage's global loads are
-// issued before the current stage multiplies.  Rows past the token count or
-// the column space are clamped to valid rows and their results discarded,
-// so no load leaves its matrix.
+// Work-group tile 128 tokens x 64 columns (so the long-context append of
+// 512 tokens x 3584 columns fills 224 of the 256 CUs).  k advances in
+// stages of 64.  Both tiles of a stage are staged through two LDS buffers
+// (rows padded to 72 elements so the 16 rows an MFMA operand load touches
+// fall in distinct banks) by loads that each cover 8 rows x 128 B, whole
+// cache lines: a load in MFMA operand order (16 rows x 64 B) halves the L1
+// throughput.  Every thread keeps the global loads of the next D stages in
+// flight.  Eight waves, two a SIMD (one wave alone cannot keep the matrix
+// pipe busy across the per-stage barrier): wave w owns tokens
+// 32 (w % 4) .. +31 against all 64 columns (2 x 4 tiles of 16 x 16) and the
+// k half w / 4 of every stage; at the end the upper k half's sums are added
+// to the lower half's through LDS (a fixed order).  Work-group ids that are
+// equal mod 8 run on one XCD; the id -> tile map gives each XCD a contiguous
+// run of tiles with the token tiles of one column tile adjacent, so that
+// column tile of L is fetched into the XCD's L2 once.  Rows past the token
+// count or the column space are clamped to valid rows and their results
+// discarded, so no load leaves its matrix.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kBM = 128;                  // tokens a work-group
-constexpr int kBN = 128;                  // columns a work-group
+constexpr int kBN = 64;                   // columns a work-group
 constexpr int kBK = 64;                   // k a stage
+constexpr int kThreads = 512;
 constexpr int kLdsRow = kBK + 8;          // padded LDS row (elements)
 constexpr int kStageElems = (kBM + kBN) * kLdsRow;
+constexpr int kPieces = kBK / 8;                    // 16-byte pieces a row a stage
+constexpr int kRowsPerPass = kThreads / kPieces;      // rows one pass of all threads covers
+constexpr int kALoads = kBM / kRowsPerPass;          // 16-byte x loads a thread a stage
+constexpr int kBLoads = kBN / kRowsPerPass;          // 16-byte L loads a thread a stage
+constexpr int kStageBytes = 2 * kStageElems * 2;    // both buffers
+constexpr int kExchBytes = 4 * 2 * 4 * 64 * 16;     // k-half exchange: 4 waves x 8 tiles x 64 lanes
+constexpr int kLdsBytes = kStageBytes > kExchBytes ? kStageBytes : kExchBytes;
 
-__global__ __launch_bounds__(256) void append_mfma(const bf16* __restrict__ x,
-                                                   const bf16* __restrict__ LkT,
-                                                   const bf16* __restrict__ LvT,
-                                                   const int64_t* __restrict__ slot,
-                                                   bf16* __restrict__ pool, int n_tok, int m, int RK,
-                                                   int RKp, int rv, int64_t page_elems,
-                                                   int64_t value_base, int64_t num_pages) {
-  __shared__ __align__(16) bf16 lds[2 * kStageElems];
+template <int D>
+__global__ __launch_bounds__(kThreads, 1) void append_mfma(const bf16* __restrict__ x,
+                                                          const bf16* __restrict__ LkT,
+                                                          const bf16* __restrict__ LvT,
+                                                          const int64_t* __restrict__ slot,
+                                                          bf16* __restrict__ pool, int n_tok, int m,
+                                                          int RK, int RKp, int rv,
+                                                          int64_t page_elems, int64_t value_base,
+                                                          int64_t num_pages, int n_tok_tiles,
+                                                          int n_tiles) {
+  __shared__ __align__(16) unsigned char smem[kLdsBytes];
+  bf16* lds = reinterpret_cast<bf16*>(smem);
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 15, lq = lane >> 4;
   const int ncols = RKp + rv;
-  const int tok0 = blockIdx.y * kBM, col0 = blockIdx.x * kBN;
 
-  // global rows this thread stages: rows tid/8 + 32*i (i < 4) of the A and
-  // B tiles, 16-byte piece tid%8 of the stage's 64 k
-  const int piece = tid & 7, prow = tid >> 3;
-  const bf16* ga[4];
-  const bf16* gb[4];
+  // XCD-aware tile order: ids id, id + 8, ... (one XCD) take consecutive tiles
+  const int id = blockIdx.x;
+  const int xcd = id & 7, q = id >> 3;
+  const int per = n_tiles >> 3, extra = n_tiles & 7;
+  const int tile = xcd * per + min(xcd, extra) + q;
+  const int tok0 = (tile % n_tok_tiles) * kBM;
+  const int col0 = (tile / n_tok_tiles) * kBN;
+  const int wm = 32 * (w & 3);                        // this wave's first token
+  const int kh = w >> 2;                              // this wave's k half
+
+  // staging: rows prow + kRowsPerPass i of both tiles, 16-byte piece
+  // tid % kPieces (a wave covers 8 rows x 128 B)
+  const int piece = tid % kPieces, prow = tid / kPieces;
+  const bf16* ga[kALoads];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int t = min(tok0 + prow + 32 * i, n_tok - 1);
+  for (int i = 0; i < kALoads; ++i) {
+    const int t = min(tok0 + prow + kRowsPerPass * i, n_tok - 1);
     ga[i] = x + int64_t(t) * m + 8 * piece;
-    const int c = col0 + prow + 32 * i;
+  }
+  const bf16* gb[kBLoads];
+#pragma unroll
+  for (int i = 0; i < kBLoads; ++i) {
+    const int c = col0 + prow + kRowsPerPass * i;
     const bf16* r;
     if (c < RK)
       r = LkT + int64_t(c) * m;
@@ -152,65 +186,86 @@ __global__ __launch_bounds__(256) void append_mfma(const bf16* __restrict__ x,
       r = LvT + int64_t(min(c - RKp, rv - 1)) * m;
     gb[i] = r + 8 * piece;
   }
-  u32x4_t ra[4], rb[4];
-  auto gload = [&](int k) {
+  u32x4_t ra[D][kALoads], rb[D][kBLoads];
+  const int nst = m / kBK;
+  auto kof = [&](int st) { return min(st, nst - 1) * kBK; };   // past the end: re-read the last
+  auto gload = [&](u32x4_t (&a)[kALoads], u32x4_t (&b)[kBLoads], int st) {
+    const int k = kof(st);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ra[i] = *reinterpret_cast<const u32x4_t*>(ga[i] + k);
-      rb[i] = *reinterpret_cast<const u32x4_t*>(gb[i] + k);
-    }
-  };
-  auto lstore = [&](int buf) {
-    bf16* A = lds + buf * kStageElems;
-    bf16* B = A + kBM * kLdsRow;
+    for (int i = 0; i < kALoads; ++i) a[i] = *reinterpret_cast<const u32x4_t*>(ga[i] + k);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      *reinterpret_cast<u32x4_t*>(A + (prow + 32 * i) * kLdsRow + 8 * piece) = ra[i];
-      *reinterpret_cast<u32x4_t*>(B + (prow + 32 * i) * kLdsRow + 8 * piece) = rb[i];
-    }
+    for (int i = 0; i < kBLoads; ++i) b[i] = *reinterpret_cast<const u32x4_t*>(gb[i] + k);
   };
 
-  floatx4_t acc[4][4];
+  floatx4_t acc[2][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-  const int wm = (w >> 1) * 64, wn = (w & 1) * 64;   // this wave's 64 x 64 sub-tile
 
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  const int nst = m / kBK;
-  for (int st = 0; st < nst; ++st) {
-    const int buf = st & 1;
-    if (st + 1 < nst) gload((st + 1) * kBK);          // in flight while this stage multiplies
-    const bf16* A = lds + buf * kStageElems;
-    const bf16* B = A + kBM * kLdsRow;
+  // keep the prologue's stages in ring order, so that waiting for the
+  // oldest stage never waits for the younger ones (vmcnt counts in order)
 #pragma unroll
-    for (int ks = 0; ks < kBK / 32; ++ks) {
-      u32x4_t a[4], b[4];
+  for (int d = 0; d < D; ++d) {
+    gload(ra[d], rb[d], d);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  // nst is a multiple of D (the launcher picks D so), and D is even or 1
+  for (int st0 = 0; st0 < nst; st0 += D) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        a[i] = *reinterpret_cast<const u32x4_t*>(A + (wm + 16 * i + lr) * kLdsRow + 32 * ks + 8 * lq);
+    for (int d = 0; d < D; ++d) {
+      const int buf = (D == 1) ? (st0 & 1) : (d & 1);
+      bf16* A = lds + buf * kStageElems;
+      bf16* B = A + kBM * kLdsRow;
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        b[j] = *reinterpret_cast<const u32x4_t*>(B + (wn + 16 * j + lr) * kLdsRow + 32 * ks + 8 * lq);
+      for (int i = 0; i < kALoads; ++i)
+        *reinterpret_cast<u32x4_t*>(A + (prow + kRowsPerPass * i) * kLdsRow + 8 * piece) = ra[d][i];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < kBLoads; ++i)
+        *reinterpret_cast<u32x4_t*>(B + (prow + kRowsPerPass * i) * kLdsRow + 8 * piece) = rb[d][i];
+      gload(ra[d], rb[d], st0 + d + D);
+      __syncthreads();
+#pragma unroll
+      for (int ks = 0; ks < kBK / 64; ++ks) {
+        const int kk = (kBK / 2) * kh + 32 * ks + 8 * lq;   // this wave's k half, step ks
+        u32x4_t a[2], b[4];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+          a[i] = *reinterpret_cast<const u32x4_t*>(A + (wm + 16 * i + lr) * kLdsRow + kk);
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a[i]),
-                                                              __builtin_bit_cast(bf16x8_t, b[j]),
-                                                              acc[i][j], 0, 0, 0);
+          b[j] = *reinterpret_cast<const u32x4_t*>(B + (16 * j + lr) * kLdsRow + kk);
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a[i]),
+                                                                __builtin_bit_cast(bf16x8_t, b[j]),
+                                                                acc[i][j], 0, 0, 0);
+      }
     }
-    if (st + 1 < nst) lstore(buf ^ 1);
-    __syncthreads();
   }
+
+  // upper k half -> LDS, lower half adds it (lane-private slots, same order everywhere)
+  floatx4_t* ex = reinterpret_cast<floatx4_t*>(smem);   // [4 waves][8 tiles][64 lanes]
+  __syncthreads();                                       // staging buffers no longer read
+  if (kh == 1) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) ex[((w & 3) * 8 + i * 4 + j) * 64 + lane] = acc[i][j];
+  }
+  __syncthreads();
+  if (kh == 1) return;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] += ex[(w * 8 + i * 4 + j) * 64 + lane];
 
   // stores: lane holds tokens 4*lq + v of each token tile, column lr of each column tile
   const int64_t slot_end = num_pages * DCKV_PAGE_TOKENS;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < 2; ++i) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int t = tok0 + wm + 16 * i + 4 * lq + v;
@@ -221,7 +276,7 @@ __global__ __launch_bounds__(256) void append_mfma(const bf16* __restrict__ x,
       const int sp = int(sl % DCKV_PAGE_TOKENS);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int c = col0 + wn + 16 * j + lr;
+        const int c = col0 + 16 * j + lr;
         if (c >= ncols) continue;
         const float val = acc[i][j][v];
         if (c < RK)
@@ -233,6 +288,20 @@ __global__ __launch_bounds__(256) void append_mfma(const bf16* __restrict__ x,
       }
     }
   }
+}
+
+template <int D>
+hipError_t launch_append_mfma(const dckv_plan& p, const void* x, int32_t n_tok, const void* Lk,
+                              const void* Lv, const int64_t* slot, void* pool, int64_t num_pages,
+                              hipStream_t stream) {
+  const int ncols = p.RKp + p.rv;
+  const int n_tok_tiles = (n_tok + kBM - 1) / kBM;
+  const int n_tiles = n_tok_tiles * ((ncols + kBN - 1) / kBN);
+  hipLaunchKernelGGL(append_mfma<D>, dim3(n_tiles), dim3(kThreads), 0, stream,
+                     static_cast<const bf16*>(x), static_cast<const bf16*>(Lk),
+                     static_cast<const bf16*>(Lv), slot, static_cast<bf16*>(pool), n_tok, p.m,
+                     p.RK, p.RKp, p.rv, p.page_elems, p.value_base, num_pages, n_tok_tiles, n_tiles);
+  return hipGetLastError();
 }
 
 template <typename T>
@@ -256,13 +325,12 @@ hipError_t launch_append(const dckv_plan& p, const void* x, int32_t n_tok, const
   if (p.dtype == DCKV_F32)
     return launch_append_t<float>(p, x, n_tok, L_keys, L_value, slot, pool, num_pages, stream);
   if (p.m % kBK == 0) {
-    const int ncols = p.RKp + p.rv;
-    dim3 grid((ncols + kBN - 1) / kBN, (n_tok + kBM - 1) / kBM);
-    hipLaunchKernelGGL(append_mfma, grid, dim3(256), 0, stream, static_cast<const bf16*>(x),
-                       static_cast<const bf16*>(L_keys), static_cast<const bf16*>(L_value), slot,
-                       static_cast<bf16*>(pool), n_tok, p.m, p.RK, p.RKp, p.rv, p.page_elems,
-                       p.value_base, num_pages);
-    return hipGetLastError();
+    const int nst = p.m / kBK;
+    if (nst % 4 == 0)
+      return launch_append_mfma<4>(p, x, n_tok, L_keys, L_value, slot, pool, num_pages, stream);
+    if (nst % 2 == 0)
+      return launch_append_mfma<2>(p, x, n_tok, L_keys, L_value, slot, pool, num_pages, stream);
+    return launch_append_mfma<1>(p, x, n_tok, L_keys, L_value, slot, pool, num_pages, stream);
   }
   return launch_append_t<bf16>(p, x, n_tok, L_keys, L_value, slot, pool, num_pages, stream);
 }

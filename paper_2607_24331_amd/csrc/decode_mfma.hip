@@ -603,7 +603,7 @@ __global__ __launch_bounds__(256) void upproj(const float* __restrict__ amerged,
                                               float* __restrict__ out, int batch, int rv,
                                               HeadTables tb) {
   constexpr int RB = 8;                        // query rows a work-group
-  constexpr int U = 4;                         // loads in flight a thread
+  constexpr int U = 8;                         // R_v loads a batch (two batches in flight)
   const int kv = blockIdx.x, ct = blockIdx.y, rbk = blockIdx.z;
   const int tid = threadIdx.x;
   const int dh = tb.head_dim, n = tb.n_kv_heads * dh, qpk = tb.q_per_kv;
@@ -612,26 +612,51 @@ __global__ __launch_bounds__(256) void upproj(const float* __restrict__ amerged,
   const int nrow = min(RB, rows - row0);
   if (nrow <= 0) return;
   extern __shared__ float sa[];                // [RB][rv], then [64][RB][32] partial sums
-  for (int i = tid; i < nrow * rv; i += 256) {
-    const int q = i / rv, r = i - q * rv;
-    const int row = row0 + q;
-    const int b = row / qpk, h = kv * qpk + row % qpk;
-    sa[q * rv + r] = amerged[(int64_t(b) * tb.n_q_heads + h) * rv + r];
-  }
-  __syncthreads();
   const int c8 = tid % 4, rg = tid / 4;
   const int col = ct * 32 + 8 * c8;            // first of eight output columns
+  // d_h is a multiple of 8 on this path; threads past d_h load a valid column
+  // group and discard their sums
+  const bf16* src = Rv + int64_t(kv) * dh + min(col, dh - 8);
+  u32x4 v[U];
+  auto issue = [&](int rbase) {
+#pragma unroll
+    for (int k = 0; k < U; ++k) v[k] = load16(src + int64_t(min(rbase + 64 * k, rv - 1)) * n);
+  };
+  issue(rg);                                   // first R_v batch overlaps the staging below
+
+  // stage the merged rows, eight loads in flight a thread
+  const int total = nrow * rv;
+  for (int base = 0; base < total; base += 256 * 8) {
+    float t[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int i = base + tid + 256 * k;
+      t[k] = 0.f;
+      if (i < total) {
+        const int q = i / rv, r = i - q * rv;
+        const int row = row0 + q;
+        const int b = row / qpk, h = kv * qpk + row % qpk;
+        t[k] = amerged[(int64_t(b) * tb.n_q_heads + h) * rv + r];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int i = base + tid + 256 * k;
+      if (i < total) sa[i] = t[k];
+    }
+  }
+  __syncthreads();
   float acc[RB][8];
 #pragma unroll
   for (int q = 0; q < RB; ++q)
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[q][j] = 0.f;
-  auto fma8 = [&](const u32x4 v, int r) {
+  auto fma8 = [&](const u32x4 w, int r) {
     float f[8];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      f[2 * j] = __uint_as_float(v[j] << 16);
-      f[2 * j + 1] = __uint_as_float(v[j] & 0xFFFF0000u);
+      f[2 * j] = __uint_as_float(w[j] << 16);
+      f[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
     }
 #pragma unroll
     for (int q = 0; q < RB; ++q) {
@@ -642,17 +667,14 @@ __global__ __launch_bounds__(256) void upproj(const float* __restrict__ amerged,
       }
     }
   };
-  if (col < dh) {                              // d_h is a multiple of 8 on this path
-    const bf16* src = Rv + int64_t(kv) * dh + col;
-    int r = rg;
-    for (; r + (U - 1) * 64 < rv; r += U * 64) {
-      u32x4 v[U];
+  for (int r = rg; r < rv; r += 64 * U) {
+    u32x4 cur[U];
 #pragma unroll
-      for (int k = 0; k < U; ++k) v[k] = load16(src + int64_t(r + 64 * k) * n);
+    for (int k = 0; k < U; ++k) cur[k] = v[k];
+    if (r + 64 * U < rv) issue(r + 64 * U);    // next batch in flight while this one multiplies
 #pragma unroll
-      for (int k = 0; k < U; ++k) fma8(v[k], r + 64 * k);
-    }
-    for (; r < rv; r += 64) fma8(load16(src + int64_t(r) * n), r);
+    for (int k = 0; k < U; ++k)
+      if (r + 64 * k < rv) fma8(cur[k], r + 64 * k);
   }
   // one reduction round: every thread's 8 rows x 8 columns go to LDS, then
   // each of the 256 outputs sums its 64 rank groups in order

@@ -280,9 +280,10 @@ def test_full_workload_sampled_rows(name):
     assert max(errs) <= TOL_REL_ROW
 
 
-@pytest.mark.parametrize("hidden", [200, 512])
+@pytest.mark.parametrize("hidden", [200, 320, 384, 512])
 def test_append_bf16_both_kernels(hidden):
-    # hidden 200 (not a multiple of 32) takes the portable kernel, 512 the MFMA one
+    # hidden 200 (not a multiple of 64) takes the portable kernel; 320, 384
+    # and 512 the MFMA one with 1, 2 and 4 k stages in flight
     wl = custom_workload(name="append_h", seed=77, hidden=hidden, num_q_heads=4, num_kv_heads=4,
                          head_dim=64, group_of_kv=(0, 1, 1, 0), group_rank=(50, 61), value_rank=100,
                          dtype="bf16", batch=1, seq_lens=(130,), prefill_lens=(130,))
