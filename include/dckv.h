@@ -26,14 +26,19 @@
  *     koff_g = r_0 + ... + r_{g-1}.
  *
  * Paged cache layout (64 tokens per page; R_K = sum_g r_g; R_Kp = R_K
- * rounded up to a multiple of 32; page_elems = 64*R_Kp + 64*r_v elements of
- * the latent dtype):
+ * rounded up to a multiple of 32; r_vp = r_v rounded up to a multiple of 16;
+ * page_elems = 64*R_Kp + 64*r_vp elements of the latent dtype):
  *   key part    chunk-major: key columns in chunks of 32, each chunk holding
  *               the 64 slots one after another: (slot s, key column k) at
  *               (k/32)*2048 + s*32 + k%32; columns R_K..R_Kp-1 are written
  *               as zero by dckv_latent_append
- *   value part  rank-major [r_v][64]: (slot s, value column j) at
- *               64*R_Kp + j*64 + s
+ *   value part  tile-major: value columns in tiles of 16, each tile holding
+ *               the slot halves 0-31 and 32-63 in turn as 16 columns x 32
+ *               slots: (slot s, value column j) at 64*R_Kp + (j/16)*1024 +
+ *               (s/32)*512 + (j%16)*32 + s%32; columns r_v..r_vp-1 are
+ *               never written and never read
+ *   Either way one 16 x 32 MFMA operand tile (16 tokens x 32 key columns, or
+ *   16 value columns x 32 tokens) is one contiguous run of 512 elements.
  *   Position pos of sequence b lives in page page_table[b*max_pages + pos/64],
  *   slot pos%64.  Page p starts at element p*page_elems of the pool.
  *
@@ -107,6 +112,7 @@ typedef struct dckv_layer_desc {
 typedef struct dckv_plan_geometry {
   int32_t key_rank_total;          /* R_K = sum of r_g */
   int32_t key_width_padded;        /* R_Kp: R_K rounded up to a multiple of 32 */
+  int32_t value_width_padded;      /* r_vp: r_v rounded up to a multiple of 16 */
   int32_t value_rank;              /* r_v */
   int32_t q_per_kv;                /* H_q / H_kv */
   int32_t folded_query_len;        /* sum over query heads h of r_{g(h)} */
@@ -114,7 +120,7 @@ typedef struct dckv_plan_geometry {
   int32_t mfma_path;               /* 1 if decode uses the bf16 MFMA kernels */
   int32_t head_slices;             /* query-head slices of the MFMA path (0 otherwise) */
   int32_t decode_waves;            /* waves a decode work-group on the MFMA path (0 otherwise) */
-  int64_t page_elems;              /* elements per page: 64*R_Kp + 64*r_v */
+  int64_t page_elems;              /* elements per page: 64*R_Kp + 64*r_vp */
   int64_t value_base;              /* element offset of the value part in a page: 64*R_Kp */
   int64_t key_factor_elems;        /* elements of the concatenated R_g blocks */
 } dckv_plan_geometry;

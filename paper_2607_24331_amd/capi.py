@@ -50,6 +50,7 @@ class PlanGeometry(ctypes.Structure):
     _fields_ = [
         ("key_rank_total", ctypes.c_int32),
         ("key_width_padded", ctypes.c_int32),
+        ("value_width_padded", ctypes.c_int32),
         ("value_rank", ctypes.c_int32),
         ("q_per_kv", ctypes.c_int32),
         ("folded_query_len", ctypes.c_int32),

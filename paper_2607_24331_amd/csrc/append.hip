@@ -5,7 +5,7 @@
 // Output column space of one token: [0, R_Kp + r_v)
 //   c <  R_K          key column c           -> page key part (chunk-major)
 //   R_K <= c < R_Kp   key-row padding         -> written as zero
-//   c >= R_Kp         value column c - R_Kp   -> page value part, rank-major
+//   c >= R_Kp         value column c - R_Kp   -> page value part, tile-major
 #include "device.h"
 #include "internal.h"
 
@@ -15,6 +15,12 @@ namespace {
 // Chunk-major key part: column c of slot s at (c/32)*2048 + s*32 + c%32.
 __device__ __forceinline__ int64_t key_elem(int s, int c) {
   return int64_t(c >> 5) * (32 * DCKV_PAGE_TOKENS) + s * 32 + (c & 31);
+}
+
+// Tile-major value part (from the value base): column j of slot s at
+// (j/16)*1024 + (s/32)*512 + (j%16)*32 + s%32.
+__device__ __forceinline__ int64_t value_elem(int s, int j) {
+  return int64_t(j >> 4) * (16 * DCKV_PAGE_TOKENS) + (s >> 5) * 512 + (j & 15) * 32 + (s & 31);
 }
 
 constexpr int kTileTok = 64;
@@ -95,7 +101,7 @@ __global__ __launch_bounds__(256) void append_valu(const T* __restrict__ x, cons
       else if (c < RKp)
         pg[key_elem(s, c)] = from_f32<T>(0.f);
       else
-        pg[value_base + int64_t(c - RKp) * DCKV_PAGE_TOKENS + s] = from_f32<T>(acc[i][j]);
+        pg[value_base + value_elem(s, c - RKp)] = from_f32<T>(acc[i][j]);
     }
   }
 }
@@ -284,7 +290,7 @@ __global__ __launch_bounds__(kThreads, 1) void append_mfma(const bf16* __restric
         else if (c < RKp)
           pg[key_elem(sp, c)] = static_cast<bf16>(0.f);
         else
-          pg[value_base + int64_t(c - RKp) * DCKV_PAGE_TOKENS + sp] = static_cast<bf16>(val);
+          pg[value_base + value_elem(sp, c - RKp)] = static_cast<bf16>(val);
       }
     }
   }

@@ -113,8 +113,9 @@ __global__ __launch_bounds__(kThreads) void split_valu(
       if (j < rv) {
         float a = acc[i] * alpha;
         if (valid) {
-          const T* vrow = pg + value_base + int64_t(j) * DCKV_PAGE_TOKENS;
-          for (int t = 0; t < n; ++t) a = fmaf(ps[t], to_f32(vrow[t]), a);
+          // tile-major values: column j of slot t at (j/16)*1024 + (t/32)*512 + (j%16)*32 + t%32
+          const T* vcol = pg + value_base + int64_t(j >> 4) * 1024 + (j & 15) * 32;
+          for (int t = 0; t < n; ++t) a = fmaf(ps[t], to_f32(vcol[(t >> 5) * 512 + (t & 31)]), a);
         }
         acc[i] = a;
       }

@@ -217,7 +217,7 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
   // two kinds: its page and kind are set once per block, and each issue is a
   // single unconditional 16-byte buffer load (out-of-range offsets read 0).
   const int lane_key = 2 * (lr * 32 + 8 * lq);        // byte offsets of this lane
-  const int lane_val = 2 * (lr * 64 + 8 * lq);
+  const int lane_val = 2 * (lr * 32 + 8 * lq);
   const int page_bytes = int(page_elems * 2);
   const int blocks_pp = (NK + NV) / RING;             // producer blocks a page
   int prod_block = 0;                                 // producer block counter over the split
@@ -235,9 +235,10 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
     r.idx0 = blk * RING;                              // first item of the block
     r.kind = page >= np ? 2 : (r.idx0 < NK ? 0 : 1);
     // key chunk c holds the 64 slots contiguously (2048 elements); M-tile m
-    // of it is the 512-element run starting at m * 512
+    // of it is the 512-element run starting at m * 512.  Value tile u (16
+    // ranks) holds the two 32-token halves as 512-element runs from u * 1024.
     r.base = r.kind == 0 ? 2 * (2048 * (kc0_w + r.idx0 / MPW) + 512 * mb_w)
-                         : 2 * (int(value_base) + 16 * (mt0_w + (r.idx0 - NK) / 2) * 64);
+                         : 2 * (int(value_base) + 1024 * (mt0_w + (r.idx0 - NK) / 2));
     return r;
   };
   // issue item s (compile-time slot) of producer block pb
@@ -251,7 +252,7 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
       off = ok ? o : kOutOfRange;
     } else if (pb.kind == 1) {
       const int mtl = (pb.idx0 - NK + s) >> 1;
-      const int o = pb.base + 2 * (16 * (s >> 1) * 64 + 32 * (s & 1)) + lane_val;
+      const int o = pb.base + 2 * (1024 * (s >> 1) + 512 * (s & 1)) + lane_val;
       const bool ok = (mtl < mcnt_w) & (16 * (mt0_w + mtl) + lr < rv) & (32 * (s & 1) + 8 * lq < pb.nval);
       off = ok ? o : kOutOfRange;
     }

@@ -68,7 +68,7 @@ struct DecodeShape {
 
 struct dckv_plan {
   int32_t m, Hq, Hkv, dh, G, rv, dtype, split_tokens, head_slices, decode_waves;
-  int32_t RK, RKp, qpk, qlen;
+  int32_t RK, RKp, rvp, qpk, qlen;
   int64_t page_elems, value_base, key_factor_elems;
   std::vector<int32_t> group_of_kv, ranks, hg, pos_in_group, koff, qoff;
   std::vector<int64_t> roff;

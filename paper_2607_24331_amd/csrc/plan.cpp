@@ -175,7 +175,8 @@ int dckv_plan_create(const dckv_layer_desc* d, dckv_plan** out) {
     p->RK = acc;
     p->RKp = (acc + 31) / 32 * 32;              // whole 32-column key chunks
     p->key_factor_elems = racc;
-    p->page_elems = int64_t(DCKV_PAGE_TOKENS) * p->RKp + int64_t(DCKV_PAGE_TOKENS) * p->rv;
+    p->rvp = (p->rv + 15) / 16 * 16;            // whole 16-column value tiles
+    p->page_elems = int64_t(DCKV_PAGE_TOKENS) * p->RKp + int64_t(DCKV_PAGE_TOKENS) * p->rvp;
     p->value_base = int64_t(DCKV_PAGE_TOKENS) * p->RKp;
     p->qpk = p->Hq / Hkv;
     p->qoff.resize(p->Hq + 1);
@@ -228,6 +229,7 @@ int dckv_plan_info(const dckv_plan* p, dckv_plan_geometry* geo, int32_t* koff,
   if (geo) {
     geo->key_rank_total = p->RK;
     geo->key_width_padded = p->RKp;
+    geo->value_width_padded = p->rvp;
     geo->value_rank = p->rv;
     geo->q_per_kv = p->qpk;
     geo->folded_query_len = p->qlen;

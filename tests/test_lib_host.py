@@ -45,6 +45,7 @@ def test_bookkeeping_matches_oracle(name):
     assert info["roff"] == bk.roff
     assert geo["key_rank_total"] == bk.key_rank_total
     assert geo["key_width_padded"] == olayout.key_width_padded(bk.key_rank_total)
+    assert geo["value_width_padded"] == olayout.value_width_padded(bk.value_rank)
     assert geo["page_elems"] == olayout.page_elems(bk.key_rank_total, bk.value_rank)
     assert geo["value_base"] == olayout.value_base(bk.key_rank_total)
     assert geo["q_per_kv"] == bk.q_per_kv

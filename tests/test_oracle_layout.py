@@ -9,8 +9,11 @@ from oracle import layout
 @pytest.mark.parametrize("RK, rv", [(1, 1), (7, 3), (8, 8), (43, 17), (128, 128), (1228, 1536)])
 def test_offsets_are_a_bijection_onto_the_page(RK, rv):
     RKp = layout.key_width_padded(RK)
+    rvp = layout.value_width_padded(rv)
     assert RKp % 32 == 0 and RK <= RKp < RK + 32
+    assert rvp % 16 == 0 and rv <= rvp < rv + 16
     n = layout.page_elems(RK, rv)
+    assert n == 64 * (RKp + rvp)
     used = np.zeros(n, dtype=np.int64)
     s = np.arange(64)[:, None]
     used_k = layout.key_offset(s, np.arange(RK)[None, :], RK).ravel()
@@ -18,29 +21,40 @@ def test_offsets_are_a_bijection_onto_the_page(RK, rv):
     np.add.at(used, used_k, 1)
     np.add.at(used, used_v, 1)
     # every latent element has its own slot; the only unused slots are the
-    # key padding columns RK..RKp-1 of every token
+    # key padding columns RK..RKp-1 and value padding columns rv..rvp-1
     assert used.max() == 1
     pad = np.flatnonzero(used == 0)
-    expect_pad = layout.key_offset(s, np.arange(RK, RKp)[None, :], RK).ravel()
+    expect_pad = np.concatenate([layout.key_offset(s, np.arange(RK, RKp)[None, :], RK).ravel(),
+                                 layout.value_offset(s, np.arange(rv, rvp)[None, :], RK).ravel()])
     assert np.array_equal(np.sort(pad), np.sort(expect_pad))
 
 
 def test_hand_offsets():
-    # R_K = 40 -> two chunks of 32 (64 padded columns); r_v = 3
+    # R_K = 40 -> two chunks of 32 (64 padded columns); r_v = 3 -> one tile of 16
     assert layout.key_width_padded(40) == 64
-    assert layout.page_elems(40, 3) == 64 * 64 + 64 * 3
+    assert layout.value_width_padded(3) == 16
+    assert layout.page_elems(40, 3) == 64 * 64 + 64 * 16
     assert layout.key_offset(0, 0, 40) == 0
     assert layout.key_offset(0, 31, 40) == 31
     assert layout.key_offset(1, 0, 40) == 32           # next slot, same chunk
     assert layout.key_offset(2, 33, 40) == 2048 + 2 * 32 + 1   # second chunk
     assert layout.value_offset(0, 0, 40) == 4096
-    assert layout.value_offset(5, 2, 40) == 4096 + 2 * 64 + 5
+    assert layout.value_offset(5, 2, 40) == 4096 + 2 * 32 + 5          # first half of tile 0
+    assert layout.value_offset(33, 2, 40) == 4096 + 512 + 2 * 32 + 1   # second half
+    assert layout.value_offset(33, 17, 40) == 4096 + 1024 + 512 + 32 + 1   # tile 1
 
 
 def test_mfma_tile_is_contiguous():
     # 16 consecutive slots x one 32-column chunk occupy 1 KB of bf16 in one run
     offs = layout.key_offset(np.arange(16, 32)[:, None], np.arange(64, 96)[None, :], 100)
     assert np.array_equal(np.sort(offs.ravel()), np.arange(offs.min(), offs.min() + 512))
+
+
+def test_value_mfma_tile_is_contiguous():
+    # 16 value columns of one tile x 32 slots of one half: 1 KB of bf16 in one run
+    for j0, s0 in ((0, 0), (16, 32), (48, 0)):
+        offs = layout.value_offset(np.arange(s0, s0 + 32)[None, :], np.arange(j0, j0 + 16)[:, None], 100)
+        assert np.array_equal(np.sort(offs.ravel()), np.arange(offs.min(), offs.min() + 512))
 
 
 def test_pack_unpack_through_permuted_pages():
