@@ -120,6 +120,10 @@ typedef struct dckv_plan_geometry {
   int32_t mfma_path;               /* 1 if decode uses the bf16 MFMA kernels */
   int32_t head_slices;             /* query-head slices of the MFMA path (0 otherwise) */
   int32_t decode_waves;            /* waves a decode work-group on the MFMA path (0 otherwise) */
+  int32_t decode_ring;             /* 16-byte loads in flight a wave on the MFMA path (12 or
+                                      16: the depth that pads the slowest wave's key and
+                                      value loads of a page least; 0 otherwise) */
+  int32_t value_tiles_per_wave;    /* 16-rank value tiles a wave on the MFMA path (0 otherwise) */
   int64_t page_elems;              /* elements per page: 64*R_Kp + 64*r_vp */
   int64_t value_base;              /* element offset of the value part in a page: 64*R_Kp */
   int64_t key_factor_elems;        /* elements of the concatenated R_g blocks */

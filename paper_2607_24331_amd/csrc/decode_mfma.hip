@@ -698,12 +698,11 @@ __global__ __launch_bounds__(256) void upproj(const float* __restrict__ amerged,
   }
 }
 
-template <int W, int NT, int MTW>
+template <int W, int NT, int MTW, int RING>
 hipError_t launch_split(const dckv_plan& p, const DecodeShape& sh, const u32x4* qblk,
                         const void* pool, int64_t num_pages, const int32_t* page_table,
                         int32_t max_pages, const int32_t* seq_lens, float* part_ml, float* part,
                         size_t lds, hipStream_t stream) {
-  constexpr int RING = 16;
   auto kern = split_mfma<W, NT, MTW, RING>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
@@ -716,18 +715,34 @@ hipError_t launch_split(const dckv_plan& p, const DecodeShape& sh, const u32x4* 
   return hipGetLastError();
 }
 
+template <int W, int NT, int MTW>
+hipError_t launch_split_r(const dckv_plan& p, const DecodeShape& sh, const u32x4* qt,
+                          const void* pool, int64_t num_pages, const int32_t* page_table,
+                          int32_t max_pages, const int32_t* seq_lens, float* part_ml, float* part,
+                          size_t lds, hipStream_t stream) {
+  if (p.mfma.ring == 12)
+    return launch_split<W, NT, MTW, 12>(p, sh, qt, pool, num_pages, page_table, max_pages,
+                                        seq_lens, part_ml, part, lds, stream);
+  return launch_split<W, NT, MTW, 16>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens,
+                                      part_ml, part, lds, stream);
+}
+
 template <int W, int NT>
 hipError_t launch_split_w(const dckv_plan& p, const DecodeShape& sh, const u32x4* qt,
                           const void* pool, int64_t num_pages, const int32_t* page_table,
                           int32_t max_pages, const int32_t* seq_lens, float* part_ml, float* part,
                           size_t lds, hipStream_t stream) {
-  const int mtw = p.mfma.mtw;
-  if (mtw <= 8)
-    return launch_split<W, NT, 8>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, lds, stream);
-  if (mtw <= 16)
-    return launch_split<W, NT, 16>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, lds, stream);
-  if (NT == 1 && mtw <= 32)
-    return launch_split<W, NT, (NT == 1 ? 32 : 16)>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, lds, stream);
+#define DCKV_SPLIT(M)                                                                   \
+  return launch_split_r<W, NT, M>(p, sh, qt, pool, num_pages, page_table, max_pages, \
+                                  seq_lens, part_ml, part, lds, stream)
+  switch (p.mfma.mtw_t) {
+    case 6: DCKV_SPLIT(6);
+    case 8: DCKV_SPLIT(8);
+    case 12: DCKV_SPLIT(12);
+    case 16: DCKV_SPLIT(16);
+    case 32: DCKV_SPLIT(NT == 1 ? 32 : 16);   // the plan takes 32 only with one head tile
+  }
+#undef DCKV_SPLIT
   return hipErrorInvalidValue;
 }
 

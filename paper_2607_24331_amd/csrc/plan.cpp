@@ -83,6 +83,35 @@ void build_mfma_tables(dckv_plan& p) {
   t.waves = p.decode_waves ? p.decode_waves : (t.mt_v >= 8 ? 8 : 4);
   t.mtw = (t.mt_v + t.waves - 1) / t.waves;
   if (t.nt * t.mtw > 32) return;               // beyond 128 accumulator registers a lane
+  t.mtw_t = 0;
+  for (int32_t c : {6, 8, 12, 16, 32})
+    if (t.mtw <= c && t.nt * c <= 32) {
+      t.mtw_t = c;
+      break;
+    }
+  if (t.mtw_t == 0) return;
+  // Ring depth: every wave's key items and the value items of a page are
+  // padded to whole rings, and the slowest wave sets the pace between the
+  // two softmax barriers of a page, so take the depth with the fewest
+  // padded items for the slowest wave (the deeper ring on a tie).
+  {
+    const int32_t sw = std::min(4 * t.nt, t.waves), mpw = 4 * t.nt / sw;
+    int32_t best = 0, best_cost = 0;
+    for (int32_t ring : {16, 12}) {
+      int32_t nk_max = 0;
+      for (int32_t s = 0; s < J; ++s)
+        for (int32_t n = 0; n < t.nt; ++n) {
+          const int32_t nk = (t.kc1[s][n] - t.kc0[s][n]) * mpw;
+          nk_max = std::max(nk_max, (nk + ring - 1) / ring * ring);
+        }
+      const int32_t cost = nk_max + (2 * t.mtw_t + ring - 1) / ring * ring;
+      if (best == 0 || cost < best_cost) {
+        best = ring;
+        best_cost = cost;
+      }
+    }
+    t.ring = best;
+  }
   const int64_t lds = int64_t(max_pairs) * 2048 + 32 * 72 * 2 + 2 * 8 * 32 * 4 + 256 * 4;
   if (lds > 160 * 1024) return;
   p.mfma_ok = true;
@@ -237,6 +266,8 @@ int dckv_plan_info(const dckv_plan* p, dckv_plan_geometry* geo, int32_t* koff,
     geo->mfma_path = p->mfma_ok ? 1 : 0;
     geo->head_slices = p->mfma_ok ? p->mfma.n_slices : 0;
     geo->decode_waves = p->mfma_ok ? p->mfma.waves : 0;
+    geo->decode_ring = p->mfma_ok ? p->mfma.ring : 0;
+    geo->value_tiles_per_wave = p->mfma_ok ? p->mfma.mtw : 0;
     geo->page_elems = p->page_elems;
     geo->value_base = p->value_base;
     geo->key_factor_elems = p->key_factor_elems;

@@ -131,6 +131,50 @@ def test_small_decode_all_rows(name):
     assert max(errs) <= TOL_REL_ROW
 
 
+# (case, decode_waves, head_slices): launch shapes of the MFMA decode beyond
+# the defaults -- 4 and 8 waves, one and two 16-head tiles, both ring depths,
+# value-tile capacities 6, 8 and 32 -- each checked on every row
+LAUNCH_SHAPES = [("gqa_uneven", 4, 0), ("gqa_uneven", 8, 2), ("singletons", 4, 0),
+                 ("mha32_two_tiles", 4, 0), ("mha32_two_tiles", 4, 2), ("valu_bf16", 8, 2),
+                 ("single_group", 4, 0)]
+
+
+@pytest.mark.parametrize("name, waves, slices", LAUNCH_SHAPES)
+def test_decode_launch_shapes(name, waves, slices):
+    from paper_2607_24331_amd import Plan
+    wl, inp, split = _small_inputs(name)
+    plan = Plan(wl.hidden, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_of_kv,
+                wl.group_rank, wl.value_rank, wl.dtype, split, slices, waves)
+    geo = plan.geometry
+    assert geo["mfma_path"] == 1 and geo["decode_waves"] == waves
+    print(f"[shape] {name} waves {waves} slices {geo['head_slices']} ring {geo['decode_ring']} "
+          f"tiles/wave {geo['value_tiles_per_wave']}", flush=True)
+    pool = gpu_pool_with_append(inp, plan)
+    out = run_decode(inp, plan, pool)
+    ref = _all_rows(inp)
+    errs = []
+    for (b, h), o in ref.items():
+        if wl.seq_lens[b] == 0:
+            assert np.all(out[b, h] == 0)
+            continue
+        errs.append(row_rel_err(out[b, h], o))
+    _report(f"{name}/w{waves}/j{slices}", errs)
+    assert max(errs) <= TOL_REL_ROW
+
+
+def test_launch_shapes_cover_both_rings():
+    from paper_2607_24331_amd import Plan
+    rings, caps = set(), set()
+    for name, waves, slices in LAUNCH_SHAPES:
+        wl, _, split = _small_inputs(name)
+        geo = Plan(wl.hidden, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_of_kv,
+                   wl.group_rank, wl.value_rank, wl.dtype, split, slices, waves).geometry
+        rings.add(geo["decode_ring"])
+        caps.add(geo["value_tiles_per_wave"])
+    assert rings == {12, 16}
+    assert max(caps) > 16 and min(caps) <= 6
+
+
 def test_peaked_softmax():
     wl, inp, split = _small_inputs("gqa_uneven")
     plan = plan_for(wl, split)
