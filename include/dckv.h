@@ -199,11 +199,12 @@ int dckv_decode(const dckv_plan* plan, const float* q, int32_t batch, const void
                 const void* R_value, float* out, void* workspace, size_t workspace_bytes,
                 void* stream);
 
-/* Benchmark instrumentation (not part of the method).  With non-NULL
- * hipEvent_t handles, every later dckv_decode on this plan records `before`
- * on its stream immediately before the split-K attention kernel (the
- * dominant kernel of a decode) and `after` immediately after it, so the
- * caller can time that kernel alone; NULL handles switch this off.  The
+/* Benchmark instrumentation (not part of the method).  With two non-NULL
+ * hipEvent_t handles, every later dckv_decode on this plan launches its
+ * split-K attention kernel (the dominant kernel of a decode) with `before`
+ * and `after` as the dispatch's own start and stop events
+ * (hipExtLaunchKernel), so their interval is that kernel's execution alone;
+ * NULL handles switch this off.  The
  * events stay owned by the caller.  A plan being instrumented must not be
  * used by several threads at once.  Makes no HIP call itself. */
 int dckv_plan_set_profile_events(dckv_plan* plan, void* before, void* after);

@@ -189,14 +189,19 @@ hipError_t launch_decode_t(const dckv_plan& p, const DecodeShape& sh, const floa
                      static_cast<const T*>(R_keys), qt, p.tables, scale);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (p.prof_before && (e = hipEventRecord(p.prof_before, stream)) != hipSuccess) return e;
-  hipLaunchKernelGGL(split_valu<T>, dim3(sh.n_split, p.Hq, sh.batch), dim3(kThreads), 0, stream, qt,
-                     static_cast<const T*>(pool), num_pages, page_table, max_pages, seq_lens,
-                     sh.max_context, sh.split_tokens, sh.n_split, p.rv, p.page_elems,
-                     p.value_base, ml, acc, p.tables);
+  if (p.prof_before && p.prof_after)   // events stamped by the kernel's own dispatch
+    hipExtLaunchKernelGGL(split_valu<T>, dim3(sh.n_split, p.Hq, sh.batch), dim3(kThreads), 0u,
+                          stream, p.prof_before, p.prof_after, 0u, qt, static_cast<const T*>(pool),
+                          num_pages, page_table, max_pages, seq_lens, sh.max_context,
+                          sh.split_tokens, sh.n_split, p.rv, p.page_elems, p.value_base, ml, acc,
+                          p.tables);
+  else
+    hipLaunchKernelGGL(split_valu<T>, dim3(sh.n_split, p.Hq, sh.batch), dim3(kThreads), 0, stream,
+                       qt, static_cast<const T*>(pool), num_pages, page_table, max_pages, seq_lens,
+                       sh.max_context, sh.split_tokens, sh.n_split, p.rv, p.page_elems,
+                       p.value_base, ml, acc, p.tables);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (p.prof_after && (e = hipEventRecord(p.prof_after, stream)) != hipSuccess) return e;
   hipLaunchKernelGGL(merge_upproject<T>, dim3(p.Hq, sh.batch), dim3(kThreads), 0, stream, ml, acc,
                      static_cast<const T*>(R_value), out, sh.n_split, p.rv, p.tables);
   return hipGetLastError();

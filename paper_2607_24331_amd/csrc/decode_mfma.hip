@@ -708,10 +708,17 @@ hipError_t launch_split(const dckv_plan& p, const DecodeShape& sh, const u32x4* 
                                      hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
   if (e != hipSuccess) return e;
   const int grid = sh.n_units * p.mfma.n_slices;
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(W * 64), lds, stream, qblk,
-                     static_cast<const bf16*>(pool), num_pages, page_table, max_pages, seq_lens,
-                     sh.max_context, sh.split_tokens, sh.n_split, sh.batch * sh.n_split, p.RK,
-                     p.rv, p.page_elems, p.value_base, part_ml, part, p.mfma);
+  if (p.prof_before && p.prof_after)   // events stamped by the kernel's own dispatch
+    hipExtLaunchKernelGGL(kern, dim3(grid), dim3(W * 64), uint32_t(lds), stream, p.prof_before,
+                          p.prof_after, 0u, qblk, static_cast<const bf16*>(pool), num_pages,
+                          page_table, max_pages, seq_lens, sh.max_context, sh.split_tokens,
+                          sh.n_split, sh.batch * sh.n_split, p.RK, p.rv, p.page_elems,
+                          p.value_base, part_ml, part, p.mfma);
+  else
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(W * 64), lds, stream, qblk,
+                       static_cast<const bf16*>(pool), num_pages, page_table, max_pages, seq_lens,
+                       sh.max_context, sh.split_tokens, sh.n_split, sh.batch * sh.n_split, p.RK,
+                       p.rv, p.page_elems, p.value_base, part_ml, part, p.mfma);
   return hipGetLastError();
 }
 
@@ -771,7 +778,6 @@ hipError_t launch_decode_mfma(const dckv_plan& p, const DecodeShape& sh, const f
                      0, stream, q, static_cast<const bf16*>(R_keys), qt, scale, p.tables, p.mfma);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (p.prof_before && (e = hipEventRecord(p.prof_before, stream)) != hipSuccess) return e;
   if (p.mfma.waves == 4)
     e = p.mfma.nt == 1
             ? launch_split_w<4, 1>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, lds, stream)
@@ -781,7 +787,6 @@ hipError_t launch_decode_mfma(const dckv_plan& p, const DecodeShape& sh, const f
             ? launch_split_w<8, 1>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, lds, stream)
             : launch_split_w<8, 2>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, lds, stream);
   if (e != hipSuccess) return e;
-  if (p.prof_after && (e = hipEventRecord(p.prof_after, stream)) != hipSuccess) return e;
   if (p.mfma.nt == 1)
     hipLaunchKernelGGL(merge_mfma<16>, dim3(sh.n_rchunks, sh.batch * p.mfma.n_slices), dim3(256), 0,
                        stream, part_ml, part, seq_lens, sh.max_context, sh.split_tokens,
