@@ -12,7 +12,12 @@ Per query head h of sequence b with T_b cached tokens:
 
 Readings where the paper is silent: softmax scale 1/sqrt(d_h); no positional
 transform of keys; no mask (the decode query sees all T_b cached tokens);
-T_b = 0 gives a zero output.  Long sequences are handled in token chunks:
+T_b = 0 gives a zero output.
+
+Several queries per sequence (speculative verification, chunked prefill):
+the Q new tokens already occupy the last Q cache positions, query i sits at
+position T_b - Q + i and sees every position up to its own (a causal mask
+inside the chunk); a query that sees no position gives a zero output.  Long sequences are handled in token chunks:
 pass one rebuilds keys chunk by chunk to get every score, pass two rebuilds
 values chunk by chunk for the weighted sum -- the same arithmetic, in less
 memory.
@@ -120,4 +125,34 @@ def decode(q: np.ndarray, pool: np.ndarray, page_table: np.ndarray, seq_lens: Se
         Zk, Zv = _layout.unpack(pool, page_table, b, T, book.key_rank_total, book.value_rank)
         for h in heads:
             out[b, h] = decode_head(q[b, h], Zk, Zv, R_keys, R_value, book, h, chunk=chunk)
+    return out
+
+
+def visible_tokens(T: int, Q: int, i: int) -> int:
+    """Cache positions query i of Q sees in a sequence of T cached tokens."""
+    return max(0, min(T, T - Q + i + 1))
+
+
+def decode_multi(q: np.ndarray, pool: np.ndarray, page_table: np.ndarray,
+                 seq_lens: Sequence[int], R_keys, R_value, book: Book,
+                 rows: Optional[Iterable[Tuple[int, int, int]]] = None,
+                 chunk: Optional[int] = 16384) -> np.ndarray:
+    """Outputs [B, Q, H_q, d_h] (fp64) of Q queries per sequence, q [B, Q, H_q, d_h].
+
+    With `rows`, only those (sequence, query, head) rows are computed; the
+    others are left NaN."""
+    B, Q, Hq, d = q.shape
+    out = np.full((B, Q, Hq, d), np.nan) if rows is not None else np.zeros((B, Q, Hq, d))
+    todo = (list(rows) if rows is not None
+            else [(b, i, h) for b in range(B) for i in range(Q) for h in range(Hq)])
+    by_seq = {}
+    for b, i, h in todo:
+        by_seq.setdefault(b, []).append((i, h))
+    for b, qh in sorted(by_seq.items()):
+        T = int(seq_lens[b])
+        Zk, Zv = _layout.unpack(pool, page_table, b, T, book.key_rank_total, book.value_rank)
+        for i, h in qh:
+            n = visible_tokens(T, Q, i)
+            out[b, i, h] = decode_head(q[b, i, h], Zk[:n], Zv[:n], R_keys, R_value, book, h,
+                                       chunk=chunk)
     return out

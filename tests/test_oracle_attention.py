@@ -268,3 +268,62 @@ def test_flat_and_blocked_factor_forms_agree():
     a = attention.decode(q, pool, tbl, lens, R_blocks, R_v, bk)
     b = attention.decode(q, pool, tbl, lens, flat, R_v, bk)
     np.testing.assert_array_equal(a, b)
+
+
+# ---------------------------------------------------- several queries a sequence
+def _reference_sdpa_causal_tail(c, qm):
+    """Causal attention over the whole sequence with the last Q query rows
+    replaced by qm[b] (Q x H_q x d); returns those Q rows."""
+    bk = c["bk"]
+    H_q, H_kv, d = bk.num_q_heads, bk.num_kv_heads, bk.head_dim
+    Q = qm.shape[1]
+    out = np.zeros(qm.shape)
+    for b, x in enumerate(c["xs"]):
+        T = x.shape[0]
+        K = torch.from_numpy(x @ c["W_k"]).view(T, H_kv, d).permute(1, 0, 2)
+        V = torch.from_numpy(x @ c["W_v"]).view(T, H_kv, d).permute(1, 0, 2)
+        K = K.repeat_interleave(H_q // H_kv, dim=0).contiguous()
+        V = V.repeat_interleave(H_q // H_kv, dim=0).contiguous()
+        qq = torch.zeros(H_q, T, d, dtype=torch.float64)
+        qq[:, T - Q:, :] = torch.from_numpy(qm[b]).permute(1, 0, 2)
+        o = torch.nn.functional.scaled_dot_product_attention(qq, K, V, is_causal=True)
+        out[b] = o[:, T - Q:, :].permute(1, 0, 2).numpy()
+    return out
+
+
+@pytest.mark.parametrize("case, Q", [(CASES[0], 3), (CASES[1], 5), (CASES[3], 8)])
+def test_multi_query_equals_causal_attention_tail(case, Q):
+    c = _full_rank_case(4321, *case)
+    bk = c["bk"]
+    g = np.random.default_rng(8)
+    qm = g.standard_normal((len(c["lens"]), Q, bk.num_q_heads, bk.head_dim))
+    got = attention.decode_multi(qm, c["pool"], c["table"], c["lens"], c["R_blocks"], c["R_v"],
+                                 bk, chunk=None)
+    np.testing.assert_allclose(got, _reference_sdpa_causal_tail(c, qm), rtol=1e-10, atol=1e-11)
+
+
+def test_multi_query_special_cases():
+    c = _full_rank_case(77, *CASES[1])
+    bk = c["bk"]
+    g = np.random.default_rng(2)
+    B, Q = len(c["lens"]), 4
+    qm = g.standard_normal((B, Q, bk.num_q_heads, bk.head_dim))
+    got = attention.decode_multi(qm, c["pool"], c["table"], c["lens"], c["R_blocks"], c["R_v"],
+                                 bk, chunk=None)
+    # the last query sees the whole sequence: the single-query decode
+    last = attention.decode(qm[:, -1], c["pool"], c["table"], c["lens"], c["R_blocks"], c["R_v"],
+                            bk, chunk=None)
+    np.testing.assert_allclose(got[:, -1], last, rtol=1e-12, atol=1e-13)
+    # sequence 1 holds 5 tokens: query 0 of 4 sees 2 of them, and with Q > T
+    # the first queries see nothing
+    assert attention.visible_tokens(5, 4, 0) == 2 and attention.visible_tokens(5, 8, 2) == 0
+    qm8 = g.standard_normal((B, 8, bk.num_q_heads, bk.head_dim))
+    got8 = attention.decode_multi(qm8, c["pool"], c["table"], c["lens"], c["R_blocks"], c["R_v"],
+                                  bk, chunk=None)
+    assert np.all(got8[1, :3] == 0) and np.all(np.abs(got8[1, 3:]).sum(axis=-1) > 0)
+    # a query that sees one token returns that token's value (T = 5, Q = 8, i = 3)
+    V = c["xs"][1] @ c["W_v"]
+    for h in range(bk.num_q_heads):
+        kv = h // (bk.num_q_heads // bk.num_kv_heads)
+        np.testing.assert_allclose(got8[1, 3, h], V[0, kv * bk.head_dim:(kv + 1) * bk.head_dim],
+                                   rtol=1e-10, atol=1e-12)
