@@ -69,6 +69,7 @@ extern "C" {
 #define DCKV_MAX_HEAD_DIM 256  /* d_h limit */
 #define DCKV_MAX_VALUE_RANK 4096
 #define DCKV_MAX_GROUP_RANK 4096
+#define DCKV_MAX_QUERIES 64     /* queries a sequence in one decode call */
 
 typedef enum {
   DCKV_OK = 0,
@@ -99,9 +100,12 @@ typedef struct dckv_layer_desc {
   int32_t split_tokens;            /* context tokens per decode work split; a
                                       multiple of 64, or 0 to choose per call from
                                       (batch, max_context) */
-  int32_t head_slices;             /* query-head slices served by separate decode
-                                      work-groups (bf16 path); 0 for the default
-                                      (one slice per 32 heads) */
+  int32_t head_slices;             /* slices of the (query, head) rows served by
+                                      separate decode work-groups (bf16 path); 0 for
+                                      the default (one slice per 32 rows) */
+  int32_t queries_per_seq;         /* Q: queries a sequence in one decode call (0 or 1:
+                                      plain decode; more: speculative verification or
+                                      chunked prefill), at most DCKV_MAX_QUERIES */
   int32_t decode_waves;            /* waves of a bf16 decode work-group: 4 or 8,
                                       or 0 for the default (eight when every wave
                                       gets at least one 16-rank value tile, i.e.
@@ -119,6 +123,7 @@ typedef struct dckv_plan_geometry {
   int32_t split_tokens;            /* tokens per decode split as described (0: per call) */
   int32_t mfma_path;               /* 1 if decode uses the bf16 MFMA kernels */
   int32_t head_slices;             /* query-head slices of the MFMA path (0 otherwise) */
+  int32_t queries_per_seq;         /* Q of the plan (at least 1) */
   int32_t decode_waves;            /* waves a decode work-group on the MFMA path (0 otherwise) */
   int32_t decode_ring;             /* 16-byte loads in flight a wave on the MFMA path (12 or
                                       16: the depth that pads the slowest wave's key and
@@ -175,8 +180,13 @@ int dckv_latent_append(const dckv_plan* plan, const void* x, int32_t n_tok,
                        const void* L_keys, const void* L_value, const int64_t* slot,
                        void* pool, int64_t num_pages, void* stream);
 
-/* Decode attention for one query per sequence over the compressed cache.
- *   q           device fp32 [batch, H_q, d_h]
+/* Decode attention over the compressed cache for Q = queries_per_seq
+ * queries per sequence (Q = 1: plain decode).  The Q new tokens already
+ * occupy the last Q cache positions of their sequence: query i sits at
+ * position seq_len - Q + i and attends to every position up to and including
+ * its own (a causal mask inside the chunk); a query that sees no position
+ * gets zeros.
+ *   q           device fp32 [batch, Q, H_q, d_h]
  *   pool        device, laid out as above (num_pages pages)
  *   page_table  device int32 [batch, max_pages]; entries outside
  *               [0, num_pages) are treated as empty pages (no fault, their
@@ -186,13 +196,13 @@ int dckv_latent_append(const dckv_plan* plan, const void* x, int32_t n_tok,
  *   R_keys      device, the R_g blocks back to back, each [r_g, h_g*d_h]
  *               row-major, group 0 first (key_factor_elems in total)
  *   R_value     device [r_v, H_kv*d_h] row-major
- *   out         device fp32 [batch, H_q, d_h]; a sequence of length 0 gets zeros
+ *   out         device fp32 [batch, Q, H_q, d_h]; a sequence of length 0 gets zeros
  *   workspace   device scratch of at least dckv_decode_workspace_bytes(batch,
  *               max_context) bytes, 256-byte aligned; its contents on entry
  *               do not matter and are overwritten
  * Results are bitwise reproducible for a fixed plan and inputs: the work
  * split depends only on split_tokens and every reduction runs in a fixed
- * order.  batch == 0 is a no-op. */
+ * order.  batch == 0 is a no-op; batch * Q is at most 65535. */
 int dckv_decode(const dckv_plan* plan, const float* q, int32_t batch, const void* pool,
                 int64_t num_pages, const int32_t* page_table, int32_t max_pages,
                 const int32_t* seq_lens, int32_t max_context, const void* R_keys,

@@ -42,6 +42,7 @@ class LayerDesc(ctypes.Structure):
         ("latent_dtype", ctypes.c_int32),
         ("split_tokens", ctypes.c_int32),
         ("head_slices", ctypes.c_int32),
+        ("queries_per_seq", ctypes.c_int32),
         ("decode_waves", ctypes.c_int32),
     ]
 
@@ -57,6 +58,7 @@ class PlanGeometry(ctypes.Structure):
         ("split_tokens", ctypes.c_int32),
         ("mfma_path", ctypes.c_int32),
         ("head_slices", ctypes.c_int32),
+        ("queries_per_seq", ctypes.c_int32),
         ("decode_waves", ctypes.c_int32),
         ("decode_ring", ctypes.c_int32),
         ("value_tiles_per_wave", ctypes.c_int32),

@@ -46,16 +46,19 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const float* __restrict_
 }
 
 // ------------------------------------------------- split (portable VALU)
-// One 256-thread block per (split, query head, sequence).  Scores: 4 threads
-// per token, each summing a quarter of the group's rank.  Values: each thread
-// owns value columns tid, tid+256, ...
+// One 256-thread block per (split, query head, query row): query row
+// bq = b * Q + i is query i of sequence b, which sees the first
+// T_b - Q + i + 1 cache positions (causal inside the chunk of Q).  Scores:
+// 4 threads per token, each summing a quarter of the group's rank.  Values:
+// each thread owns value columns tid, tid+256, ...
 template <typename T>
 __global__ __launch_bounds__(kThreads) void split_valu(
     const float* __restrict__ qt, const T* __restrict__ pool, int64_t num_pages,
     const int32_t* __restrict__ page_table, int max_pages, const int32_t* __restrict__ seq_lens,
     int max_context, int split_tokens, int n_split, int rv, int64_t page_elems,
     int64_t value_base, float* __restrict__ part_ml, float* __restrict__ part_acc, HeadTables tb) {
-  const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int split = blockIdx.x, h = blockIdx.y, bq = blockIdx.z;
+  const int b = bq / tb.n_queries, qi = bq % tb.n_queries;
   const int tid = threadIdx.x;
   __shared__ float qs[DCKV_MAX_GROUP_RANK];
   __shared__ float part[4][DCKV_PAGE_TOKENS];
@@ -63,11 +66,12 @@ __global__ __launch_bounds__(kThreads) void split_valu(
 
   int T_b = seq_lens[b];
   T_b = T_b < 0 ? 0 : (T_b > max_context ? max_context : T_b);
+  const int T_q = max(0, T_b - tb.n_queries + qi + 1);   // positions this query sees
   const int t0 = split * split_tokens;
-  const int t1 = min(t0 + split_tokens, T_b);
+  const int t1 = min(t0 + split_tokens, T_q);
   const int r = tb.rank_of_q[h];
   const int koff = tb.koff_of_q[h];
-  for (int j = tid; j < r; j += kThreads) qs[j] = qt[int64_t(b) * tb.qlen + tb.qoff[h] + j];
+  for (int j = tid; j < r; j += kThreads) qs[j] = qt[int64_t(bq) * tb.qlen + tb.qoff[h] + j];
   __syncthreads();
 
   float acc[kAccPerThread];
@@ -124,7 +128,7 @@ __global__ __launch_bounds__(kThreads) void split_valu(
     __syncthreads();
   }
 
-  const int64_t row = (int64_t(b) * tb.n_q_heads + h) * n_split + split;
+  const int64_t row = (int64_t(bq) * tb.n_q_heads + h) * n_split + split;
   if (tid == 0) {
     part_ml[row * 2 + 0] = m_run;
     part_ml[row * 2 + 1] = l_run;
@@ -185,24 +189,25 @@ hipError_t launch_decode_t(const dckv_plan& p, const DecodeShape& sh, const floa
   float* ml = reinterpret_cast<float*>(ws + sh.off_ml);
   float* acc = reinterpret_cast<float*>(ws + sh.off_acc);
   const float scale = kLog2e / std::sqrt(float(p.dh));
-  hipLaunchKernelGGL(fold_kernel<T>, dim3(p.Hq, sh.batch), dim3(kThreads), 0, stream, q,
+  const int rows = sh.batch * p.Q;               // query rows (sequence, query)
+  hipLaunchKernelGGL(fold_kernel<T>, dim3(p.Hq, rows), dim3(kThreads), 0, stream, q,
                      static_cast<const T*>(R_keys), qt, p.tables, scale);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (p.prof_before && p.prof_after)   // events stamped by the kernel's own dispatch
-    hipExtLaunchKernelGGL(split_valu<T>, dim3(sh.n_split, p.Hq, sh.batch), dim3(kThreads), 0u,
+    hipExtLaunchKernelGGL(split_valu<T>, dim3(sh.n_split, p.Hq, rows), dim3(kThreads), 0u,
                           stream, p.prof_before, p.prof_after, 0u, qt, static_cast<const T*>(pool),
                           num_pages, page_table, max_pages, seq_lens, sh.max_context,
                           sh.split_tokens, sh.n_split, p.rv, p.page_elems, p.value_base, ml, acc,
                           p.tables);
   else
-    hipLaunchKernelGGL(split_valu<T>, dim3(sh.n_split, p.Hq, sh.batch), dim3(kThreads), 0, stream,
+    hipLaunchKernelGGL(split_valu<T>, dim3(sh.n_split, p.Hq, rows), dim3(kThreads), 0, stream,
                        qt, static_cast<const T*>(pool), num_pages, page_table, max_pages, seq_lens,
                        sh.max_context, sh.split_tokens, sh.n_split, p.rv, p.page_elems,
                        p.value_base, ml, acc, p.tables);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(merge_upproject<T>, dim3(p.Hq, sh.batch), dim3(kThreads), 0, stream, ml, acc,
+  hipLaunchKernelGGL(merge_upproject<T>, dim3(p.Hq, rows), dim3(kThreads), 0, stream, ml, acc,
                      static_cast<const T*>(R_value), out, sh.n_split, p.rv, p.tables);
   return hipGetLastError();
 }
@@ -229,7 +234,7 @@ DecodeShape decode_shape(const dckv_plan& p, int32_t batch, int32_t max_context)
   s.split_tokens = int32_t(L);
   s.n_split = max_context > 0 ? int32_t((max_context + L - 1) / L) : 1;
   s.off_qt = 0;
-  s.off_ml = align_up(size_t(batch) * p.qlen * sizeof(float), 256);
+  s.off_ml = align_up(size_t(batch) * p.Q * p.qlen * sizeof(float), 256);
   if (s.mfma)   // the MFMA path keeps hi/lo query blocks of 2 KB per (sequence, slice, chunk)
     s.off_ml = align_up(size_t(batch) * p.mfma.n_slices * p.mfma.max_pairs * 2048, 256);
   if (s.mfma) {
@@ -240,9 +245,9 @@ DecodeShape decode_shape(const dckv_plan& p, int32_t batch, int32_t max_context)
     const size_t rows = size_t(batch) * p.mfma.n_slices * s.n_split;
     s.off_acc = s.off_ml + align_up(rows * 2 * nh * sizeof(float), 256);
     s.off_opart = s.off_acc + align_up(rows * nh * size_t(p.rv) * sizeof(float), 256);
-    s.bytes = s.off_opart + align_up(size_t(batch) * p.Hq * p.rv * sizeof(float), 256);
+    s.bytes = s.off_opart + align_up(size_t(batch) * p.Q * p.Hq * p.rv * sizeof(float), 256);
   } else {
-    const size_t rows = size_t(batch) * p.Hq * s.n_split;
+    const size_t rows = size_t(batch) * p.Q * p.Hq * s.n_split;
     s.off_acc = s.off_ml + align_up(rows * 2 * sizeof(float), 256);
     s.off_opart = s.off_acc + align_up(rows * p.rv * sizeof(float), 256);
     s.bytes = s.off_opart;

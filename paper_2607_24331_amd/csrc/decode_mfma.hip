@@ -101,15 +101,16 @@ __global__ __launch_bounds__(64) void fold_blocks(const float* __restrict__ q,
                                                   const bf16* __restrict__ Rk,
                                                   u32x4* __restrict__ qblk_ws, float scale,
                                                   HeadTables tb, MfmaTables mt) {
-  const int pr = blockIdx.x, j = blockIdx.y;
+  const int j = blockIdx.y, pr = blockIdx.z;           // (sequence, slice) on x: grid x is wide
   const int J = mt.n_slices;
-  const int b = blockIdx.z / J, slice = blockIdx.z % J;
+  const int b = blockIdx.x / J, slice = blockIdx.x % J;
   const int nch0 = mt.kc1[slice][0] - mt.kc0[slice][0];
   const int npairs = nch0 + (mt.nt > 1 ? mt.kc1[slice][1] - mt.kc0[slice][1] : 0);
   if (pr >= npairs) return;
   const int n = pr < nch0 ? 0 : 1;
   const int c = mt.kc0[slice][n] + pr - (n ? nch0 : 0);
-  const int h = mt.hord[slice][16 * n + j];
+  const int row = mt.hord[slice][16 * n + j];           // query i * H_q + head h, or -1
+  const int h = row < 0 ? -1 : row % tb.n_q_heads, qi = row < 0 ? 0 : row / tb.n_q_heads;
   const int lane = threadIdx.x, kk = lane & 31, half = lane >> 5;
   const int k = 32 * c + kk;
   const int dh = tb.head_dim, hd = dh / 2, d0 = half * hd;   // d_h is a multiple of 8
@@ -118,7 +119,7 @@ __global__ __launch_bounds__(64) void fold_blocks(const float* __restrict__ q,
     const int lo = tb.koff_of_q[h], r = tb.rank_of_q[h];
     if (k >= lo && k < lo + r) {
       const bf16* row = Rk + tb.roff_of_q[h] + int64_t(k - lo) * tb.rstride_of_q[h] + tb.rcol_of_q[h] + d0;
-      const float* qh = q + (int64_t(b) * tb.n_q_heads + h) * dh + d0;
+      const float* qh = q + ((int64_t(b) * tb.n_queries + qi) * tb.n_q_heads + h) * dh + d0;
       // 8 columns a step: one 8-byte-aligned load of R (4 x bf16 pairs) and two float4 of q
       for (int d = 0; d < hd; d += 8) {
         uint32_t w4[4];
@@ -208,6 +209,13 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
   const int mt0_w = w * mt.mtw;
   const int mcnt_w = max(0, min(mt.mtw, mt.mt_v - mt0_w));
   const int kc_last = mt.kc1[slice][n_w] - 1;
+  // causal limit of this lane's score column: query i of Q sits at position
+  // T_b - Q + i and sees the positions before it and its own
+  int lim = T_b;
+  if (scoring) {
+    const int row = mt.hord[slice][16 * n_w + lr];
+    if (row >= 0) lim = T_b - mt.queries + row / mt.q_heads + 1;
+  }
   const int kvalid_last = min(8, max(0, RK - (32 * kc_last + 8 * lq)));
 
   // ---- producer.  The item stream of a page is NK key items (chunk-major,
@@ -336,7 +344,7 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const int tok = 16 * (mb_w + m) + 4 * lq + v;
-          if (!pvalid || tok >= nval) S[m][v] = -INFINITY;
+          if (!pvalid || tok >= nval || t0 + 64 * page + tok >= lim) S[m][v] = -INFINITY;
           tmax = fmaxf(tmax, S[m][v]);
         }
       tmax = wave_max16(tmax);
@@ -457,7 +465,7 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
 
 // ---------------------------------------------------------------------------
 // Merge: a[b][h][r] = sum_s 2^(m_s - M) acc_s[r] / sum_s 2^(m_s - M) l_s.
-// Grid (value-rank chunks of kMergeRanks, batch * slices), 256 threads.
+// Grid (batch * slices, value-rank chunks of kMergeRanks), 256 threads.
 // Pass 1: per head slot the maximum M and the weighted sum L over splits,
 // read from the compact (m, l) rows, eight independent loads a thread.
 // Pass 2: a split row of the chunk is kMergeRanks * NH contiguous floats;
@@ -475,8 +483,8 @@ __global__ __launch_bounds__(256) void merge_mfma(const float* __restrict__ part
   constexpr int TPR = kMergeRanks * NH / 4;   // threads a split row
   constexpr int G = 256 / TPR;                // split groups
   constexpr int SUB = 256 / NH;               // split groups of pass 1
-  const int rc = blockIdx.x;
-  const int bj = blockIdx.y;
+  const int bj = blockIdx.x;                  // (sequence, slice) on x: grid x is wide
+  const int rc = blockIdx.y;
   const int J = mt.n_slices;
   const int b = bj / J, slice = bj % J;
   const int tid = threadIdx.x;
@@ -585,17 +593,17 @@ __global__ __launch_bounds__(256) void merge_mfma(const float* __restrict__ part
     const float tv[4] = {t.x, t.y, t.z, t.w};
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      const int h = mt.hord[slice][hq + k];
-      if (h >= 0)
-        amerged[(int64_t(b) * tb.n_q_heads + h) * rv + r] =
+      const int row = mt.hord[slice][hq + k];           // query i * H_q + head h
+      if (row >= 0)
+        amerged[(int64_t(b) * tb.n_queries * tb.n_q_heads + row) * rv + r] =
             sM[hq + k] == -INFINITY ? 0.f : tv[k] * sInvL[hq + k];
     }
   }
 }
 
 // Up-projection o[b][h][:] = a[b][h][:] R_v[:, kv(h) block] (Sec. III-A z R,
-// Sec. III-D R_v).  Grid (KV heads, column tiles of 32, row blocks of 8): a
-// work-group serves every query row (sequence, head) of its KV head in its row
+// Sec. III-D R_v).  Grid (row blocks of 8, KV heads, column tiles of 32): a
+// work-group serves every query row (sequence, query, head) of its KV head in its row
 // block, for 32 output columns.  Thread t: 8 columns (one 16-byte load a
 // rank), rank group t/4 (ranks t/4, t/4 + 64, ...), four loads in flight; the
 // 64 rank groups are then summed in a fixed order, one query row a round.
@@ -605,7 +613,7 @@ __global__ __launch_bounds__(256) void upproj(const float* __restrict__ amerged,
                                               HeadTables tb) {
   constexpr int RB = 8;                        // query rows a work-group
   constexpr int U = 8;                         // R_v loads a batch (two batches in flight)
-  const int kv = blockIdx.x, ct = blockIdx.y, rbk = blockIdx.z;
+  const int rbk = blockIdx.x, kv = blockIdx.y, ct = blockIdx.z;   // row blocks on x: grid x is wide
   const int tid = threadIdx.x;
   const int dh = tb.head_dim, n = tb.n_kv_heads * dh, qpk = tb.q_per_kv;
   const int rows = batch * qpk;
@@ -774,7 +782,7 @@ hipError_t launch_decode_mfma(const dckv_plan& p, const DecodeShape& sh, const f
   float* amerged = reinterpret_cast<float*>(ws + sh.off_opart);
   const size_t lds = mfma_split_lds_bytes(p);
   const float scale = kLog2e / std::sqrt(float(p.dh));
-  hipLaunchKernelGGL(fold_blocks, dim3(p.mfma.max_pairs, 16, sh.batch * p.mfma.n_slices), dim3(64),
+  hipLaunchKernelGGL(fold_blocks, dim3(sh.batch * p.mfma.n_slices, 16, p.mfma.max_pairs), dim3(64),
                      0, stream, q, static_cast<const bf16*>(R_keys), qt, scale, p.tables, p.mfma);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -788,22 +796,22 @@ hipError_t launch_decode_mfma(const dckv_plan& p, const DecodeShape& sh, const f
             : launch_split_w<8, 2>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, lds, stream);
   if (e != hipSuccess) return e;
   if (p.mfma.nt == 1)
-    hipLaunchKernelGGL(merge_mfma<16>, dim3(sh.n_rchunks, sh.batch * p.mfma.n_slices), dim3(256), 0,
+    hipLaunchKernelGGL(merge_mfma<16>, dim3(sh.batch * p.mfma.n_slices, sh.n_rchunks), dim3(256), 0,
                        stream, part_ml, part, seq_lens, sh.max_context, sh.split_tokens,
                        sh.n_split, p.rv, amerged, p.tables, p.mfma);
   else
-    hipLaunchKernelGGL(merge_mfma<32>, dim3(sh.n_rchunks, sh.batch * p.mfma.n_slices), dim3(256), 0,
+    hipLaunchKernelGGL(merge_mfma<32>, dim3(sh.batch * p.mfma.n_slices, sh.n_rchunks), dim3(256), 0,
                        stream, part_ml, part, seq_lens, sh.max_context, sh.split_tokens,
                        sh.n_split, p.rv, amerged, p.tables, p.mfma);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  const int rows = sh.batch * p.qpk;
+  const int rows = sh.batch * p.Q * p.qpk;            // (sequence, query, head of a KV head)
   const size_t lds_up = (size_t(8) * p.rv + 64 * 8 * 32) * sizeof(float);
   e = hipFuncSetAttribute(reinterpret_cast<const void*>(upproj),
                           hipFuncAttributeMaxDynamicSharedMemorySize, int(lds_up));
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(upproj, dim3(p.Hkv, (p.dh + 31) / 32, (rows + 7) / 8), dim3(256), lds_up,
-                     stream, amerged, static_cast<const bf16*>(R_value), out, sh.batch, p.rv,
-                     p.tables);
+  hipLaunchKernelGGL(upproj, dim3((rows + 7) / 8, p.Hkv, (p.dh + 31) / 32), dim3(256), lds_up,
+                     stream, amerged, static_cast<const bf16*>(R_value), out, sh.batch * p.Q,
+                     p.rv, p.tables);
   return hipGetLastError();
 }
 

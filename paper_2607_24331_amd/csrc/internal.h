@@ -18,6 +18,7 @@ struct HeadTables {
   int32_t head_dim;
   int32_t q_per_kv;
   int32_t n_groups;
+  int32_t n_queries;                         // Q: queries a sequence
   int32_t qlen;                              // sum over heads of r_{g(h)}
   int32_t qoff[DCKV_MAX_HEADS + 1];          // folded-query offset of head h
   int32_t rank_of_q[DCKV_MAX_HEADS];         // r_{g(h)}
@@ -27,7 +28,7 @@ struct HeadTables {
   int64_t roff_of_q[DCKV_MAX_HEADS];         // element offset of R_g
 };
 
-constexpr int kMaxSlices = 4;     // head slices of the MFMA decode path
+constexpr int kMaxSlices = 8;     // (query, head) row slices of the MFMA decode path
 constexpr int kSliceHeads = 32;   // at most two 16-head MFMA tiles per slice
 
 // Schedule of the MFMA decode path (bf16 latents), fixed by the plan.  Query
@@ -37,6 +38,8 @@ constexpr int kSliceHeads = 32;   // at most two 16-head MFMA tiles per slice
 // read by exactly one work-group.
 struct MfmaTables {
   int32_t n_slices;                        // J
+  int32_t q_heads;                         // H_q
+  int32_t queries;                         // Q: queries a sequence
   int32_t nt;                              // 16-head MFMA tiles per slice (1 or 2)
   int32_t mt_v;                            // value M-tiles: ceil(r_v / 16)
   int32_t waves;                           // waves a work-group: 4 or 8
@@ -44,8 +47,8 @@ struct MfmaTables {
   int32_t mtw_t;                           // compiled tile capacity: 6, 8, 12, 16 or 32 >= mtw
   int32_t ring;                            // loads in flight a wave (12 or 16)
   int32_t max_pairs;                       // most LDS query blocks of any slice
-  int32_t slice_heads[kMaxSlices];         // real heads in slice s
-  int32_t hord[kMaxSlices][kSliceHeads];   // head slot -> query head, -1 for padding
+  int32_t slice_heads[kMaxSlices];         // real rows in slice s
+  int32_t hord[kMaxSlices][kSliceHeads];   // slot -> row i * H_q + h (query i, head h), -1 padding
   int32_t kc0[kMaxSlices][2];              // first 32-column key chunk of (slice, tile)
   int32_t kc1[kMaxSlices][2];              // one past the last
 };
@@ -69,7 +72,7 @@ struct DecodeShape {
 }  // namespace dckv
 
 struct dckv_plan {
-  int32_t m, Hq, Hkv, dh, G, rv, dtype, split_tokens, head_slices, decode_waves;
+  int32_t m, Hq, Hkv, dh, G, rv, dtype, split_tokens, head_slices, decode_waves, Q;
   int32_t RK, RKp, rvp, qpk, qlen;
   int64_t page_elems, value_base, key_factor_elems;
   std::vector<int32_t> group_of_kv, ranks, hg, pos_in_group, koff, qoff;

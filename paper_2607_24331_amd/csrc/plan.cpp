@@ -37,31 +37,39 @@ void build_mfma_tables(dckv_plan& p) {
   if (p.dtype != DCKV_BF16) return;
   if (p.dh % 8 != 0) return;                   // the up-projection reads 8 columns at a time
   MfmaTables& t = p.mfma;
-  // Query heads ordered by (group of their KV head, head index): the heads
-  // of one group are adjacent, so a tile's key columns are one range.
-  std::vector<int32_t> order(p.Hq);
-  for (int32_t h = 0; h < p.Hq; ++h) order[h] = h;
+  // Rows (query i, head h), numbered i * H_q + h, ordered by (group of the
+  // KV head, head, query): the rows of one group are adjacent, so a tile's
+  // key columns are one range, and the queries of one head share a tile.
+  const int32_t nrows = p.Q * p.Hq;
+  std::vector<int32_t> order(nrows);
+  for (int32_t r = 0; r < nrows; ++r) order[r] = r;
   std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
-    return p.group_of_kv[a / p.qpk] < p.group_of_kv[b / p.qpk];
+    const int32_t ha = a % p.Hq, hb = b % p.Hq;
+    const int32_t ga = p.group_of_kv[ha / p.qpk], gb = p.group_of_kv[hb / p.qpk];
+    if (ga != gb) return ga < gb;
+    if (ha != hb) return ha < hb;
+    return a < b;
   });
-  int32_t J = p.head_slices > 0 ? p.head_slices : (p.Hq + kSliceHeads - 1) / kSliceHeads;
-  if (J > kMaxSlices || J > p.Hq) return;
-  const int32_t per = (p.Hq + J - 1) / J;
+  int32_t J = p.head_slices > 0 ? p.head_slices : (nrows + kSliceHeads - 1) / kSliceHeads;
+  if (J > kMaxSlices || J > nrows) return;
+  const int32_t per = (nrows + J - 1) / J;
   if (per > kSliceHeads) return;
   t.n_slices = J;
+  t.q_heads = p.Hq;
+  t.queries = p.Q;
   t.nt = (per + 15) / 16;
   int32_t max_pairs = 0;
   for (int32_t s = 0; s < J; ++s) {
-    const int32_t h0 = std::min(p.Hq, s * per), h1 = std::min(p.Hq, (s + 1) * per);
+    const int32_t h0 = std::min(nrows, s * per), h1 = std::min(nrows, (s + 1) * per);
     t.slice_heads[s] = h1 - h0;
     for (int32_t i = 0; i < kSliceHeads; ++i) t.hord[s][i] = (h0 + i < h1) ? order[h0 + i] : -1;
     int32_t pairs = 0;
     for (int32_t n = 0; n < t.nt; ++n) {
       int32_t lo = p.RK, hi = 0;
       for (int32_t i = 16 * n; i < 16 * n + 16; ++i) {
-        const int32_t h = t.hord[s][i];
-        if (h < 0) continue;
-        const int32_t g = p.group_of_kv[h / p.qpk];
+        const int32_t row = t.hord[s][i];
+        if (row < 0) continue;
+        const int32_t g = p.group_of_kv[(row % p.Hq) / p.qpk];
         lo = std::min(lo, p.koff[g]);
         hi = std::max(hi, p.koff[g] + p.ranks[g]);
       }
@@ -151,6 +159,9 @@ int dckv_plan_create(const dckv_layer_desc* d, dckv_plan** out) {
   if (d->head_slices < 0 || d->head_slices > DCKV_MAX_HEADS)
     return fail(DCKV_EINVAL, "plan_create: head_slices %d outside [0,%d]", d->head_slices,
                 DCKV_MAX_HEADS);
+  if (d->queries_per_seq < 0 || d->queries_per_seq > DCKV_MAX_QUERIES)
+    return fail(DCKV_EINVAL, "plan_create: queries_per_seq %d outside [0,%d]",
+                d->queries_per_seq, DCKV_MAX_QUERIES);
 
   const int32_t Hkv = d->num_kv_heads, G = d->num_groups, dh = d->head_dim;
   std::vector<int32_t> hg(G, 0), pos(Hkv, 0);
@@ -186,6 +197,7 @@ int dckv_plan_create(const dckv_layer_desc* d, dckv_plan** out) {
     p->split_tokens = d->split_tokens;
     p->head_slices = d->head_slices;
     p->decode_waves = d->decode_waves;
+    p->Q = d->queries_per_seq > 0 ? d->queries_per_seq : 1;
     p->group_of_kv.assign(d->group_of_kv_head, d->group_of_kv_head + Hkv);
     p->ranks.assign(d->group_rank, d->group_rank + G);
     p->hg = hg;
@@ -217,6 +229,7 @@ int dckv_plan_create(const dckv_layer_desc* d, dckv_plan** out) {
     t.head_dim = dh;
     t.q_per_kv = p->qpk;
     t.n_groups = G;
+    t.n_queries = p->Q;
     for (int32_t h = 0; h < p->Hq; ++h) {
       const int32_t kv = h / p->qpk, g = p->group_of_kv[kv];
       p->qoff[h] = qacc;
@@ -265,6 +278,7 @@ int dckv_plan_info(const dckv_plan* p, dckv_plan_geometry* geo, int32_t* koff,
     geo->split_tokens = p->split_tokens;
     geo->mfma_path = p->mfma_ok ? 1 : 0;
     geo->head_slices = p->mfma_ok ? p->mfma.n_slices : 0;
+    geo->queries_per_seq = p->Q;
     geo->decode_waves = p->mfma_ok ? p->mfma.waves : 0;
     geo->decode_ring = p->mfma_ok ? p->mfma.ring : 0;
     geo->value_tiles_per_wave = p->mfma_ok ? p->mfma.mtw : 0;
@@ -318,7 +332,8 @@ int dckv_decode(const dckv_plan* p, const float* q, int32_t batch, const void* p
   if (batch == 0) return DCKV_OK;
   if (!q || !pool || !page_table || !seq_lens || !R_keys || !R_value || !out || !workspace)
     return fail(DCKV_EINVAL, "decode: null device pointer");
-  if (batch > 65535) return fail(DCKV_EINVAL, "decode: batch %d above 65535", batch);
+  if (int64_t(batch) * p->Q > 65535)
+    return fail(DCKV_EINVAL, "decode: batch %d x queries %d above 65535", batch, p->Q);
   if (num_pages < 1) return fail(DCKV_EINVAL, "decode: num_pages %lld < 1", (long long)num_pages);
   if (max_pages < 1) return fail(DCKV_EINVAL, "decode: max_pages %d < 1", max_pages);
   if (max_context < 0 || int64_t(max_context) > int64_t(max_pages) * DCKV_PAGE_TOKENS)

@@ -43,7 +43,7 @@ class Plan:
     def __init__(self, hidden: int, num_q_heads: int, num_kv_heads: int, head_dim: int,
                  group_of_kv_head: Sequence[int], group_rank: Sequence[int], value_rank: int,
                  dtype: str = "bf16", split_tokens: int = 0, head_slices: int = 0,
-                 decode_waves: int = 0):
+                 decode_waves: int = 0, queries_per_seq: int = 1):
         if dtype not in _DTYPES:
             raise ValueError(f"dtype must be one of {sorted(_DTYPES)}")
         self.dtype = dtype
@@ -54,7 +54,7 @@ class Plan:
                               ctypes.cast(self._gmap, ctypes.POINTER(ctypes.c_int32)),
                               ctypes.cast(self._ranks, ctypes.POINTER(ctypes.c_int32)),
                               value_rank, _DTYPES[dtype][0], split_tokens, head_slices,
-                              decode_waves)
+                              queries_per_seq, decode_waves)
         handle = ctypes.c_void_p()
         _check(_lib.dckv_plan_create(ctypes.byref(desc), ctypes.byref(handle)), "plan_create")
         self._handle = handle
@@ -67,6 +67,7 @@ class Plan:
         self.page_elems = self.geometry["page_elems"]
         self.split_tokens = self.geometry["split_tokens"]
         self.key_factor_elems = self.geometry["key_factor_elems"]
+        self.queries_per_seq = self.geometry["queries_per_seq"]
 
     @property
     def handle(self) -> ctypes.c_void_p:
@@ -166,12 +167,20 @@ def decode(plan: Plan, q: torch.Tensor, pool: torch.Tensor, page_table: torch.Te
            seq_lens: torch.Tensor, max_context: int, R_keys: torch.Tensor, R_value: torch.Tensor,
            out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
            stream=None) -> torch.Tensor:
-    """Attention output [batch, H_q, d_h] (fp32) of one query per sequence."""
-    if q.dim() != 3:
-        raise ValueError("q must be [batch, H_q, d_h]")
+    """Attention output (fp32) of the plan's Q queries per sequence: q and the
+    result are [batch, Q, H_q, d_h], or [batch, H_q, d_h] when Q is 1.  Query
+    i of sequence b sits at cache position seq_len - Q + i and sees every
+    position up to its own."""
+    Q = plan.queries_per_seq
+    if q.dim() == 3 and Q == 1:
+        qshape = (q.shape[0], plan.num_q_heads, plan.head_dim)
+    elif q.dim() == 4:
+        qshape = (q.shape[0], Q, plan.num_q_heads, plan.head_dim)
+    else:
+        raise ValueError("q must be [batch, Q, H_q, d_h] (or [batch, H_q, d_h] with Q = 1)")
     B = q.shape[0]
     dt = plan.torch_dtype
-    pq = _dev(q, "q", torch.float32, (B, plan.num_q_heads, plan.head_dim))
+    pq = _dev(q, "q", torch.float32, qshape)
     pp = _dev(pool, "pool", dt)
     if page_table.dim() != 2 or page_table.shape[0] != B:
         raise ValueError("page_table must be [batch, max_pages]")
@@ -182,8 +191,8 @@ def decode(plan: Plan, q: torch.Tensor, pool: torch.Tensor, page_table: torch.Te
         raise ValueError(f"R_keys holds {R_keys.numel()} elements, expected {plan.key_factor_elems}")
     prv = _dev(R_value, "R_value", dt, (plan.value_rank, plan.num_kv_heads * plan.head_dim))
     if out is None:
-        out = torch.empty((B, plan.num_q_heads, plan.head_dim), dtype=torch.float32, device=q.device)
-    po = _dev(out, "out", torch.float32, (B, plan.num_q_heads, plan.head_dim))
+        out = torch.empty(qshape, dtype=torch.float32, device=q.device)
+    po = _dev(out, "out", torch.float32, qshape)
     need = plan.workspace_bytes(B, max_context)
     if workspace is None:
         workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=q.device)

@@ -175,6 +175,47 @@ def test_launch_shapes_cover_both_rings():
     assert max(caps) > 16 and min(caps) <= 6
 
 
+# (case, Q, latent dtype): several causal queries a sequence.  mha_odd holds
+# a one-token and an empty sequence (queries that see nothing give zeros);
+# 32 heads x 8 queries fill all eight row slices of the MFMA path; f32 runs
+# the portable kernels.
+MULTI = [("gqa_uneven", 4, "bf16"), ("mha32_two_tiles", 2, "bf16"), ("mha32_two_tiles", 8, "bf16"),
+         ("mha_odd", 8, "bf16"), ("singletons", 3, "bf16"), ("mha_odd", 3, "f32")]
+
+
+@pytest.mark.parametrize("name, Q, dtype", MULTI)
+def test_multi_query_all_rows(name, Q, dtype):
+    from paper_2607_24331_amd import Plan, decode
+    wl, inp, split = _small_inputs(name, dtype)
+    plan = Plan(wl.hidden, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_of_kv,
+                wl.group_rank, wl.value_rank, wl.dtype, split, queries_per_seq=Q)
+    geo = plan.geometry
+    assert geo["queries_per_seq"] == Q
+    assert geo["mfma_path"] == (1 if dtype == "bf16" else 0)
+    print(f"[multi] {name} Q {Q} {dtype} slices {geo['head_slices']}", flush=True)
+    pool = gpu_pool_with_append(inp, plan)
+    qm = np.random.default_rng(11).standard_normal(
+        (wl.batch, Q, wl.num_q_heads, wl.head_dim)).astype(np.float32)
+    out = decode(plan, torch.from_numpy(qm).cuda(), pool, torch.from_numpy(inp.page_table).cuda(),
+                 torch.from_numpy(inp.seq_lens).cuda(), int(max(wl.seq_lens)),
+                 dev(inp.R_keys_flat, wl.dtype), dev(inp.R_value, wl.dtype))
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().astype(np.float64)
+    ref = oattn.decode_multi(qm, oracle_pool(inp), inp.page_table, wl.seq_lens, inp.R_blocks,
+                             inp.R_value, book_for(wl), chunk=None)
+    errs = []
+    for b in range(wl.batch):
+        for i in range(Q):
+            seen = oattn.visible_tokens(wl.seq_lens[b], Q, i)
+            for h in range(wl.num_q_heads):
+                if seen == 0:
+                    assert np.all(got[b, i, h] == 0)
+                else:
+                    errs.append(row_rel_err(got[b, i, h], ref[b, i, h]))
+    _report(f"multi/{name}/Q{Q}/{dtype}", errs)
+    assert max(errs) <= (TOL_REL_ROW if dtype == "bf16" else TOL_REL_ROW_F32)
+
+
 def test_peaked_softmax():
     wl, inp, split = _small_inputs("gqa_uneven")
     plan = plan_for(wl, split)

@@ -86,17 +86,19 @@ def test_bookkeeping_random_layers():
     (dict(dtype=7), "DCKV_EDTYPE"),
     (dict(split=100), "DCKV_EINVAL"),
     (dict(head_dim=300), "DCKV_EINVAL"),
+    (dict(queries=65), "DCKV_EINVAL"),                 # above DCKV_MAX_QUERIES
+    (dict(queries=-1), "DCKV_EINVAL"),
 ])
 def test_plan_create_rejects(lib, change, status):
     a = dict(hidden=64, num_q=4, gmap=[0, 1, 0, 1], ranks=[8, 8], value_rank=16, dtype=1, split=0,
-             head_dim=16)
+             head_dim=16, queries=0)
     a.update(change)
     gm = (ctypes.c_int32 * 4)(*a["gmap"])
     rk = (ctypes.c_int32 * 2)(*a["ranks"])
     desc = capi.LayerDesc(a["hidden"], a["num_q"], 4, a["head_dim"], 2,
                           ctypes.cast(gm, ctypes.POINTER(ctypes.c_int32)),
                           ctypes.cast(rk, ctypes.POINTER(ctypes.c_int32)),
-                          a["value_rank"], a["dtype"], a["split"])
+                          a["value_rank"], a["dtype"], a["split"], 0, a["queries"])
     out = ctypes.c_void_p(12345)
     st = lib.dckv_plan_create(ctypes.byref(desc), ctypes.byref(out))
     assert capi.STATUS_NAMES[st] == status
@@ -177,3 +179,19 @@ def test_decode_path_selection():
     from paper_2607_24331_amd import Plan as P2
     p2 = P2(wl.hidden, 32, 32, 128, wl.group_of_kv, wl.group_rank, wl.value_rank, "bf16", 0, 2)
     assert p2.geometry["mfma_path"] == 1 and p2.geometry["head_slices"] == 2
+
+
+def test_queries_per_seq_plan():
+    from paper_2607_24331_amd import Plan
+    wl = make_workload("mha_long_t128k")
+    args = (wl.hidden, 32, 32, 128, wl.group_of_kv, wl.group_rank, wl.value_rank, "bf16", 0)
+    one = Plan(*args)
+    assert one.geometry["queries_per_seq"] == 1 and one.geometry["head_slices"] == 1
+    # 32 heads x 4 queries = 128 rows: four slices of 32 on the MFMA path
+    four = Plan(*args, queries_per_seq=4)
+    assert four.geometry["queries_per_seq"] == 4
+    assert four.geometry["mfma_path"] == 1 and four.geometry["head_slices"] == 4
+    # more workspace: one merged row per (sequence, query, head)
+    assert four.workspace_bytes(1, 131072) > one.workspace_bytes(1, 131072)
+    # 32 heads x 16 queries = 512 rows exceed the eight slices: portable path
+    assert Plan(*args, queries_per_seq=16).geometry["mfma_path"] == 0
