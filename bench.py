@@ -40,6 +40,9 @@ def parse():
     ap.add_argument("--split-tokens", type=int, default=0)
     ap.add_argument("--head-slices", type=int, default=0)
     ap.add_argument("--decode-waves", type=int, default=0)
+    ap.add_argument("--queries", type=int, default=1,
+                    help="causal queries a sequence in each decode (speculative verification / "
+                         "chunked prefill); 1 is plain decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one device copy of this many MiB before timing (a known-size "
@@ -49,7 +52,7 @@ def parse():
     return ap.parse_args()
 
 
-def device_inputs(wl, plan, torch):
+def device_inputs(wl, plan, torch, Q=1):
     """Synthetic device tensors of the workload's shapes (seeded)."""
     from workloads.inputs import random_pool_fill
     dev = "cuda"
@@ -67,7 +70,8 @@ def device_inputs(wl, plan, torch):
         pool=pool,
         page_table=table.to(dev),
         seq_lens=torch.tensor(wl.seq_lens, dtype=torch.int32, device=dev),
-        q=torch.randn((wl.batch, wl.num_q_heads, wl.head_dim), generator=g, device=dev),
+        q=torch.randn((wl.batch, Q, wl.num_q_heads, wl.head_dim) if Q > 1
+                      else (wl.batch, wl.num_q_heads, wl.head_dim), generator=g, device=dev),
         R_keys=(torch.randn(plan.key_factor_elems, generator=g, device=dev) * 0.05).to(tdt),
         R_value=(torch.randn((wl.value_rank, wl.kv_dim), generator=g, device=dev) * 0.02).to(tdt),
     )
@@ -123,14 +127,15 @@ def kernel_sources_sha256():
     return h.hexdigest()
 
 
-def measured_traffic(wl, launch):
+def measured_traffic(wl, launch, Q=1):
     """HBM bytes per launch of the split kernel from the committed counter
     summary (FETCH_SIZE and WRITE_SIZE, each scaled by the same counter's
     reading for a plain device copy of known size), or None when there is
     no summary for this workload and launch shape, or the kernel sources
     changed since the counters were taken."""
     root = os.path.dirname(os.path.abspath(__file__))
-    path = os.path.join(root, "profiles", f"split_mfma_{wl.name}_counters.md")
+    tag = wl.name if Q == 1 else f"{wl.name}_q{Q}"
+    path = os.path.join(root, "profiles", f"split_mfma_{tag}_counters.md")
     if not os.path.exists(path):
         return None
     keys = {}
@@ -149,10 +154,11 @@ def measured_traffic(wl, launch):
         return None
 
 
-def cpu_baseline(wl, budget_s):
+def cpu_baseline(wl, budget_s, Q=1):
     """The oracle, as it stands, on a bounded sample of the same workload:
     the append of all new tokens plus whole-context decode of as many heads
-    as fit the time budget; the step time is extrapolated to every head."""
+    as fit the time budget; the step time is extrapolated to every (sequence,
+    query, head) row."""
     import numpy as np
     from oracle import append as oappend
     from oracle import attention as oattn
@@ -186,17 +192,17 @@ def cpu_baseline(wl, budget_s):
         heads_done += 1
         if t_dec + t_app >= budget_s:
             break
-    rows = wl.batch * wl.num_q_heads
+    rows = wl.batch * Q * wl.num_q_heads
     # every (sequence, head) row of a full step costs about T_b / T_0 of a sampled row
     ctx_scale = sum(wl.seq_lens) / (wl.batch * T)
     step_s = t_app + t_dec / heads_done * rows * ctx_scale
     return {
-        "value": wl.batch / step_s,
+        "value": wl.batch * Q / step_s,
         "unit": "tokens/s",
         "cores": int(threads),
         "kind": "oracle",
         "sample": (f"oracle append of {wl.append_tokens} tokens ({t_app:.2f} s) + fp64 decode of "
-                   f"{heads_done} of {rows} (sequence, head) rows at {T} context tokens "
+                   f"{heads_done} of {rows} (sequence, query, head) rows at {T} context tokens "
                    f"({t_dec:.2f} s), extrapolated to the full step ({step_s:.1f} s)"),
     }
 
@@ -215,12 +221,13 @@ def main():
     wl = make_workload(args.workload)
     plan = Plan(wl.hidden, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_of_kv,
                 wl.group_rank, wl.value_rank, wl.dtype, args.split_tokens, args.head_slices,
-                args.decode_waves)
+                args.decode_waves, args.queries)
     mfma = bool(plan.geometry["mfma_path"])
-    inp = device_inputs(wl, plan, torch)
+    Q = args.queries
+    inp = device_inputs(wl, plan, torch, Q)
     max_ctx = max(wl.seq_lens)
     split_used = plan.split_tokens or _auto_split(plan, wl, max_ctx)
-    out = torch.empty((wl.batch, wl.num_q_heads, wl.head_dim), dtype=torch.float32, device="cuda")
+    out = torch.empty(tuple(inp["q"].shape), dtype=torch.float32, device="cuda")
     ws = plan.new_workspace(wl.batch, max_ctx)
 
     def step():
@@ -273,11 +280,15 @@ def main():
     nb = algorithmic_bytes(wl)
     launch = (f"split_tokens={split_used} head_slices={plan.geometry['head_slices']} "
               f"decode_waves={plan.geometry['decode_waves']}")
-    traffic = measured_traffic(wl, launch) if mfma else None
+    if Q > 1:
+        launch += f" queries_per_seq={Q}"
+    traffic = measured_traffic(wl, launch, Q) if mfma else None
     achieved = nb["latent"] / (kern_ms * 1e-3) / 1e9
-    value = wl.batch / (ms_step * 1e-3)
+    value = wl.batch * Q / (ms_step * 1e-3)
     rec = {
-        "metric": "compressed-KV decode attention tokens/s (achieved HBM GB/s in roofline)",
+        "metric": ("compressed-KV decode attention tokens/s (achieved HBM GB/s in roofline)" if Q == 1
+                   else f"compressed-KV causal {Q}-query attention query tokens/s "
+                        "(achieved HBM GB/s in roofline)"),
         "value": value,
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -300,6 +311,7 @@ def main():
             "latent_dtype": wl.dtype, "split_tokens": split_used,
             "head_slices": plan.geometry["head_slices"],
             "decode_waves": plan.geometry["decode_waves"],
+            "queries_per_seq": Q,
         },
         "context_tokens_per_s": sum(wl.seq_lens) / (ms_step * 1e-3),
         "step_hbm_gbs": (nb["decode_total"] + nb["append"]) / (ms_step * 1e-3) / 1e9,
@@ -319,7 +331,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
-        rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+        rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, Q)
     print(json.dumps(rec), flush=True)
 
 
