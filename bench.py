@@ -44,6 +44,10 @@ def parse():
                     help="causal queries a sequence in each decode (speculative verification / "
                          "chunked prefill); 1 is plain decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--decode-only", action="store_true",
+                    help="time the decode alone (no latent append in the step)")
+    ap.add_argument("--dense", action="store_true",
+                    help="time the uncompressed bf16 KV decode baseline on the workload's shape")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one device copy of this many MiB before timing (a known-size "
                          "kernel for scaling hardware traffic counters)")
@@ -154,7 +158,7 @@ def measured_traffic(wl, launch, Q=1):
         return None
 
 
-def cpu_baseline(wl, budget_s, Q=1):
+def cpu_baseline(wl, budget_s, Q=1, with_append=True):
     """The oracle, as it stands, on a bounded sample of the same workload:
     the append of all new tokens plus whole-context decode of as many heads
     as fit the time budget; the step time is extrapolated to every (sequence,
@@ -179,7 +183,7 @@ def cpu_baseline(wl, budget_s, Q=1):
     Zv = g.standard_normal((T, wl.value_rank), dtype=np.float32)
     q = g.standard_normal((wl.batch, wl.num_q_heads, wl.head_dim))
     t_app = 0.0
-    if wl.append_tokens:
+    if wl.append_tokens and with_append:
         x = g.standard_normal((wl.append_tokens, wl.hidden), dtype=np.float32)
         t0 = time.perf_counter()
         oappend.latents(x, L_keys, L_value, wl.dtype)
@@ -201,10 +205,115 @@ def cpu_baseline(wl, budget_s, Q=1):
         "unit": "tokens/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": (f"oracle append of {wl.append_tokens} tokens ({t_app:.2f} s) + fp64 decode of "
+        "sample": ((f"oracle append of {wl.append_tokens} tokens ({t_app:.2f} s) + "
+                    if wl.append_tokens and with_append else "") + "fp64 decode of "
                    f"{heads_done} of {rows} (sequence, query, head) rows at {T} context tokens "
                    f"({t_dec:.2f} s), extrapolated to the full step ({step_s:.1f} s)"),
     }
+
+
+def dense_cpu_baseline(wl, budget_s):
+    """The oracle's uncompressed decode, as it stands, on a bounded sample: one
+    sequence of the workload's head shape at a shorter context, extrapolated
+    linearly in context length over the whole batch."""
+    import numpy as np
+    from oracle import dense as odense
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()
+                       if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    g = np.random.default_rng(wl.seed)
+    Hkv, d = wl.num_kv_heads, wl.head_dim
+    T = min(max(wl.seq_lens), 4096)
+    table = np.arange(-(-T // 64), dtype=np.int32)[None, :]
+    pool = odense.new_pool(table.shape[1], Hkv, d)
+    odense.pack(pool, table, 0, 0, g.standard_normal((T, Hkv, d)), g.standard_normal((T, Hkv, d)))
+    q = g.standard_normal((1, wl.num_q_heads, d))
+    t0 = time.perf_counter()
+    odense.decode(q, pool, table, [T], Hkv)
+    dt = time.perf_counter() - t0
+    step_s = dt * sum(wl.seq_lens) / T
+    return {"value": wl.batch / step_s, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": (f"oracle uncompressed decode of one sequence of {T} tokens, all "
+                       f"{wl.num_q_heads} heads ({dt:.2f} s), extrapolated to "
+                       f"{sum(wl.seq_lens)} context tokens ({step_s:.1f} s)")}
+
+
+def main_dense(args, torch, wl):
+    """The uncompressed baseline: decode over a bf16 K/V cache of the workload's
+    shape, same head map, pages and timing as the compressed path."""
+    from paper_2607_24331_amd import dense_decode, dense_page_elems, dense_workspace_bytes
+    Hq, Hkv, d = wl.num_q_heads, wl.num_kv_heads, wl.head_dim
+    pe = dense_page_elems(Hkv, d)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(2000 + wl.seed)
+    pool = torch.empty((wl.total_pages, pe), dtype=torch.bfloat16, device="cuda")
+    for i in range(0, wl.total_pages, 256):       # fill in slices: no full-size fp32 temporary
+        j = min(wl.total_pages, i + 256)
+        pool[i:j] = torch.randn((j - i, pe), generator=gen, device="cuda").to(torch.bfloat16)
+    pages = wl.pages_per_seq
+    table = torch.zeros((wl.batch, wl.max_pages), dtype=torch.int32)
+    pos = 0
+    for b, n in enumerate(pages):
+        table[b, :n] = torch.arange(pos, pos + n, dtype=torch.int32)
+        pos += n
+    table = table.cuda()
+    seq_lens = torch.tensor(wl.seq_lens, dtype=torch.int32, device="cuda")
+    q = torch.randn((wl.batch, Hq, d), generator=gen, device="cuda")
+    max_ctx = max(wl.seq_lens)
+    out = torch.empty((wl.batch, Hq, d), dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(256, dense_workspace_bytes(Hq, Hkv, d, args.split_tokens, wl.batch, max_ctx)),
+                     dtype=torch.uint8, device="cuda")
+
+    def step(ev=None):
+        dense_decode(q, pool, table, seq_lens, max_ctx, Hkv, split_tokens=args.split_tokens, out=out,
+                     workspace=ws, events=ev)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    K = args.steps
+    every = max(1, args.profile_every)
+    ev = {k: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for k in range(K) if k % every == 0}
+    for a, b in ev.values():
+        a.record()
+        b.record()
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record()
+    for k in range(K):
+        step(ev.get(k))
+    t_end.record()
+    torch.cuda.synchronize()
+    ms_step = t_start.elapsed_time(t_end) / K
+    kern_ms = sum(a.elapsed_time(b) for a, b in ev.values()) / len(ev)
+    print(f"[bench] dense {wl.name}: {ms_step:.4f} ms/step, split kernel {kern_ms:.4f} ms",
+          file=sys.stderr, flush=True)
+    kv_bytes = sum(wl.seq_lens) * Hkv * d * 2 * 2
+    achieved = kv_bytes / (kern_ms * 1e-3) / 1e9
+    rec = {
+        "metric": "uncompressed bf16 KV decode attention tokens/s (baseline; achieved HBM GB/s in roofline)",
+        "value": wl.batch / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": K, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded random keys, values and queries of the workload's shapes)",
+        "config": {"workload": wl.name, "kv_cache": "uncompressed bf16", "batch": wl.batch,
+                   "context_tokens": sum(wl.seq_lens), "q_heads": Hq, "kv_heads": Hkv,
+                   "head_dim": d, "split_tokens": args.split_tokens or "auto"},
+        "context_tokens_per_s": sum(wl.seq_lens) / (ms_step * 1e-3),
+        "roofline": {"kernel": "uncompressed split-K attention (dense_split)", "bound": "hbm",
+                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None, "kernel_ms": kern_ms,
+                     "bytes_per_launch": kv_bytes, "kernel_launches_timed": len(ev)},
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = dense_cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(rec), flush=True)
 
 
 def main():
@@ -219,6 +328,8 @@ def main():
     from workloads import make_workload
 
     wl = make_workload(args.workload)
+    if args.dense:
+        return main_dense(args, torch, wl)
     plan = Plan(wl.hidden, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_of_kv,
                 wl.group_rank, wl.value_rank, wl.dtype, args.split_tokens, args.head_slices,
                 args.decode_waves, args.queries)
@@ -230,8 +341,10 @@ def main():
     out = torch.empty(tuple(inp["q"].shape), dtype=torch.float32, device="cuda")
     ws = plan.new_workspace(wl.batch, max_ctx)
 
+    append = bool(wl.append_tokens) and not args.decode_only
+
     def step():
-        if wl.append_tokens:
+        if append:
             latent_append(plan, inp["x"], inp["L_keys"], inp["L_value"], inp["slot"], inp["pool"])
         decode(plan, inp["q"], inp["pool"], inp["page_table"], inp["seq_lens"], max_ctx,
                inp["R_keys"], inp["R_value"], out=out, workspace=ws)
@@ -304,7 +417,7 @@ def main():
             "workload": wl.name,
             "batch": wl.batch,
             "context_tokens": sum(wl.seq_lens),
-            "appended_tokens": wl.append_tokens,
+            "appended_tokens": wl.append_tokens if append else 0,
             "q_heads": wl.num_q_heads, "kv_heads": wl.num_kv_heads, "head_dim": wl.head_dim,
             "hidden": wl.hidden, "group_sizes": list(wl.group_sizes),
             "group_ranks": list(wl.group_rank), "value_rank": wl.value_rank,
@@ -314,7 +427,7 @@ def main():
             "queries_per_seq": Q,
         },
         "context_tokens_per_s": sum(wl.seq_lens) / (ms_step * 1e-3),
-        "step_hbm_gbs": (nb["decode_total"] + nb["append"]) / (ms_step * 1e-3) / 1e9,
+        "step_hbm_gbs": (nb["decode_total"] + (nb["append"] if append else 0)) / (ms_step * 1e-3) / 1e9,
         "roofline": {
             "kernel": "split-K latent attention (" + ("split_mfma" if mfma else "split_valu") + ")",
             "bound": "hbm",
@@ -331,7 +444,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
-        rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, Q)
+        rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, Q, append)
     print(json.dumps(rec), flush=True)
 
 

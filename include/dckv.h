@@ -219,6 +219,32 @@ int dckv_decode(const dckv_plan* plan, const float* q, int32_t batch, const void
  * used by several threads at once.  Makes no HIP call itself. */
 int dckv_plan_set_profile_events(dckv_plan* plan, void* before, void* after);
 
+/* ------------------------------------------------------------------------
+ * Uncompressed baseline (no compression): decode over a paged bf16 K/V
+ * cache with the same head map, scale and split-K scheme, so the compressed
+ * path can be compared with the cache it replaces on the same harness.
+ * Page of 64 tokens: keys [H_kv][64][d_h] then values [H_kv][64][d_h]; key
+ * (slot s, KV head kv, column d) at (kv*64 + s)*d_h + d, the value at
+ * 64*H_kv*d_h + (kv*64 + s)*d_h + d.  Supported: d_h in {64, 128, 256}, at
+ * most 8 query heads a KV head.  split_tokens: a multiple of 64, or 0 to
+ * choose from (batch, max_context). */
+int dckv_dense_page_elems(int32_t num_kv_heads, int32_t head_dim, int64_t* elems);
+int dckv_dense_workspace_bytes(int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                               int32_t split_tokens, int32_t batch, int32_t max_context,
+                               size_t* bytes);
+/* Arguments as for dckv_decode (q and out [batch, H_q, d_h] fp32, page_table,
+ * seq_lens, max_context, workspace), plus: kv_pool, num_pages pages of the
+ * layout above.  With two non-NULL hipEvent_t handles the split kernel is
+ * launched with them as its dispatch's start and stop events (benchmark
+ * instrumentation).  Validation, ownership and error behaviour as for
+ * dckv_decode. */
+int dckv_dense_decode(int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                      int32_t split_tokens, const float* q, int32_t batch, const void* kv_pool,
+                      int64_t num_pages, const int32_t* page_table, int32_t max_pages,
+                      const int32_t* seq_lens, int32_t max_context, float* out, void* workspace,
+                      size_t workspace_bytes, void* before_event, void* after_event,
+                      void* stream);
+
 /* Message of the last failing call on this thread ("" if none). */
 const char* dckv_last_error(void);
 

@@ -69,6 +69,15 @@ struct DecodeShape {
   size_t bytes;
 };
 
+// Launch shape of one uncompressed decode call (dense.hip).
+struct DenseShape {
+  int32_t n_q_heads, n_kv_heads, head_dim, batch, max_context;
+  int32_t split_tokens;     // context tokens a work-group
+  int32_t n_split;          // ceil(max_context / split_tokens), at least 1
+  size_t off_o, off_ml;     // workspace: unnormalised outputs, then (m, l)
+  size_t bytes;
+};
+
 }  // namespace dckv
 
 struct dckv_plan {
@@ -100,6 +109,12 @@ hipError_t launch_decode_mfma(const dckv_plan& p, const DecodeShape& sh, const f
 
 // Defined in the kernel sources.
 DecodeShape decode_shape(const dckv_plan& p, int32_t batch, int32_t max_context);
+DenseShape dense_shape(int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, int32_t batch,
+                       int32_t max_context, int32_t split_tokens);
+hipError_t launch_dense_decode(const DenseShape& sh, const float* q, const void* pool,
+                               int64_t num_pages, const int32_t* page_table, int32_t max_pages,
+                               const int32_t* seq_lens, float* out, void* workspace,
+                               hipEvent_t before, hipEvent_t after, hipStream_t stream);
 hipError_t launch_append(const dckv_plan& p, const void* x, int32_t n_tok, const void* L_keys,
                          const void* L_value, const int64_t* slot, void* pool, int64_t num_pages,
                          hipStream_t stream);

@@ -353,4 +353,76 @@ int dckv_decode(const dckv_plan* p, const float* q, int32_t batch, const void* p
   return DCKV_OK;
 }
 
+// ------------------------------------------------ uncompressed baseline
+static int dense_check(const char* where, int32_t Hq, int32_t Hkv, int32_t dh, int32_t split) {
+  if (Hq < 1 || Hq > DCKV_MAX_HEADS || Hkv < 1 || Hq % Hkv != 0 || Hq / Hkv > 8)
+    return fail(DCKV_EINVAL, "%s: %d query heads over %d KV heads (need a multiple, at most 8 a KV head, %d heads in all)",
+                where, Hq, Hkv, DCKV_MAX_HEADS);
+  if (dh != 64 && dh != 128 && dh != 256)
+    return fail(DCKV_EINVAL, "%s: head_dim %d is not 64, 128 or 256", where, dh);
+  if (split < 0 || split % DCKV_PAGE_TOKENS != 0 || split > (1 << 24))
+    return fail(DCKV_EINVAL, "%s: split_tokens %d is not 0 or a positive multiple of %d", where, split,
+                DCKV_PAGE_TOKENS);
+  return DCKV_OK;
+}
+
+int dckv_dense_page_elems(int32_t num_kv_heads, int32_t head_dim, int64_t* elems) {
+  if (!elems) return fail(DCKV_EINVAL, "dense_page_elems: null output pointer");
+  if (num_kv_heads < 1 || num_kv_heads > DCKV_MAX_HEADS || head_dim < 1 || head_dim > DCKV_MAX_HEAD_DIM)
+    return fail(DCKV_EINVAL, "dense_page_elems: %d KV heads of dimension %d", num_kv_heads, head_dim);
+  *elems = int64_t(2) * DCKV_PAGE_TOKENS * num_kv_heads * head_dim;
+  return DCKV_OK;
+}
+
+int dckv_dense_workspace_bytes(int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                               int32_t split_tokens, int32_t batch, int32_t max_context,
+                               size_t* bytes) {
+  if (!bytes) return fail(DCKV_EINVAL, "dense_workspace_bytes: null bytes pointer");
+  int st = dense_check("dense_workspace_bytes", num_q_heads, num_kv_heads, head_dim, split_tokens);
+  if (st != DCKV_OK) return st;
+  if (batch < 0 || max_context < 0)
+    return fail(DCKV_EINVAL, "dense_workspace_bytes: negative batch %d or max_context %d", batch,
+                max_context);
+  *bytes = dckv::dense_shape(num_q_heads, num_kv_heads, head_dim, batch, max_context, split_tokens).bytes;
+  return DCKV_OK;
+}
+
+int dckv_dense_decode(int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                      int32_t split_tokens, const float* q, int32_t batch, const void* kv_pool,
+                      int64_t num_pages, const int32_t* page_table, int32_t max_pages,
+                      const int32_t* seq_lens, int32_t max_context, float* out, void* workspace,
+                      size_t workspace_bytes, void* before_event, void* after_event,
+                      void* stream) {
+  int st = dense_check("dense_decode", num_q_heads, num_kv_heads, head_dim, split_tokens);
+  if (st != DCKV_OK) return st;
+  if (batch < 0) return fail(DCKV_EINVAL, "dense_decode: batch %d < 0", batch);
+  if (batch == 0) return DCKV_OK;
+  if (batch > 65535) return fail(DCKV_EINVAL, "dense_decode: batch %d above 65535", batch);
+  if (!q || !kv_pool || !page_table || !seq_lens || !out || !workspace)
+    return fail(DCKV_EINVAL, "dense_decode: null device pointer");
+  if ((before_event == nullptr) != (after_event == nullptr))
+    return fail(DCKV_EINVAL, "dense_decode: give both events or neither");
+  if (num_pages < 1) return fail(DCKV_EINVAL, "dense_decode: num_pages %lld < 1", (long long)num_pages);
+  if (max_pages < 1) return fail(DCKV_EINVAL, "dense_decode: max_pages %d < 1", max_pages);
+  if (max_context < 0 || int64_t(max_context) > int64_t(max_pages) * DCKV_PAGE_TOKENS)
+    return fail(DCKV_EINVAL, "dense_decode: max_context %d outside [0, max_pages*64 = %lld]",
+                max_context, (long long)max_pages * DCKV_PAGE_TOKENS);
+  if (!aligned(q, 16) || !aligned(kv_pool, 16) || !aligned(out, 16) || !aligned(page_table, 4) ||
+      !aligned(seq_lens, 4))
+    return fail(DCKV_EALIGN, "dense_decode: q, kv_pool and out must be 16-byte aligned");
+  if (!aligned(workspace, 256)) return fail(DCKV_EALIGN, "dense_decode: workspace must be 256-byte aligned");
+  const dckv::DenseShape sh =
+      dckv::dense_shape(num_q_heads, num_kv_heads, head_dim, batch, max_context, split_tokens);
+  if (workspace_bytes < sh.bytes)
+    return fail(DCKV_EWORKSPACE, "dense_decode: workspace of %zu bytes, %zu needed", workspace_bytes,
+                sh.bytes);
+  hipError_t e = dckv::launch_dense_decode(sh, q, kv_pool, num_pages, page_table, max_pages,
+                                           seq_lens, out, workspace,
+                                           static_cast<hipEvent_t>(before_event),
+                                           static_cast<hipEvent_t>(after_event),
+                                           static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(DCKV_EHIP, "dense_decode: %s", hipGetErrorString(e));
+  return DCKV_OK;
+}
+
 }  // extern "C"

@@ -201,3 +201,56 @@ def decode(plan: Plan, q: torch.Tensor, pool: torch.Tensor, page_table: torch.Te
                             psl, int(max_context), prk, prv, po, pw, workspace.numel(),
                             _stream_handle(stream)), "decode")
     return out
+
+
+# ------------------------------------------------------ uncompressed baseline
+def dense_page_elems(num_kv_heads: int, head_dim: int) -> int:
+    """Elements of one page (64 tokens) of the uncompressed K/V cache."""
+    n = ctypes.c_int64()
+    _check(_lib.dckv_dense_page_elems(num_kv_heads, head_dim, ctypes.byref(n)), "dense_page_elems")
+    return n.value
+
+
+def dense_workspace_bytes(num_q_heads: int, num_kv_heads: int, head_dim: int, split_tokens: int,
+                          batch: int, max_context: int) -> int:
+    n = ctypes.c_size_t()
+    _check(_lib.dckv_dense_workspace_bytes(num_q_heads, num_kv_heads, head_dim, split_tokens, batch,
+                                           int(max_context), ctypes.byref(n)),
+           "dense_workspace_bytes")
+    return n.value
+
+
+def dense_decode(q: torch.Tensor, kv_pool: torch.Tensor, page_table: torch.Tensor,
+                 seq_lens: torch.Tensor, max_context: int, num_kv_heads: int,
+                 split_tokens: int = 0, out: Optional[torch.Tensor] = None,
+                 workspace: Optional[torch.Tensor] = None, events=None, stream=None) -> torch.Tensor:
+    """Uncompressed decode (the baseline): q [batch, H_q, d_h] fp32 over a
+    bf16 pool of pages [H_kv][64][d_h] keys then values; returns [batch, H_q,
+    d_h] fp32.  `events`, a pair of torch.cuda.Event, stamp the split
+    kernel's dispatch."""
+    if q.dim() != 3:
+        raise ValueError("q must be [batch, H_q, d_h]")
+    B, Hq, d = q.shape
+    pq = _dev(q, "q", torch.float32, (B, Hq, d))
+    pe = dense_page_elems(num_kv_heads, d)
+    pp = _dev(kv_pool, "kv_pool", torch.bfloat16)
+    if kv_pool.numel() % pe:
+        raise ValueError("kv_pool size is not a whole number of pages")
+    if page_table.dim() != 2 or page_table.shape[0] != B:
+        raise ValueError("page_table must be [batch, max_pages]")
+    pt = _dev(page_table, "page_table", torch.int32)
+    psl = _dev(seq_lens, "seq_lens", torch.int32, (B,))
+    if out is None:
+        out = torch.empty((B, Hq, d), dtype=torch.float32, device=q.device)
+    po = _dev(out, "out", torch.float32, (B, Hq, d))
+    if workspace is None:
+        need = dense_workspace_bytes(Hq, num_kv_heads, d, split_tokens, B, max_context)
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=q.device)
+    pw = _dev(workspace, "workspace", torch.uint8)
+    eb = events[0].cuda_event if events else None
+    ea = events[1].cuda_event if events else None
+    _check(_lib.dckv_dense_decode(Hq, num_kv_heads, d, split_tokens, pq, B, pp,
+                                  kv_pool.numel() // pe, pt, page_table.shape[1], psl,
+                                  int(max_context), po, pw, workspace.numel(), eb, ea,
+                                  _stream_handle(stream)), "dense_decode")
+    return out
