@@ -129,6 +129,10 @@ typedef struct dckv_plan_geometry {
                                       16: the depth that pads the slowest wave's key and
                                       value loads of a page least; 0 otherwise) */
   int32_t value_tiles_per_wave;    /* 16-rank value tiles a wave on the MFMA path (0 otherwise) */
+  int32_t key_chunk_loads;         /* 32-column key chunks the MFMA path loads a 64-token page,
+                                      summed over its 16-row tiles: a tile loads the chunks of
+                                      its rows' groups, so a group cut by a tile boundary is
+                                      loaded twice (0 otherwise) */
   int64_t page_elems;              /* elements per page: 64*R_Kp + 64*r_vp */
   int64_t value_base;              /* element offset of the value part in a page: 64*R_Kp */
   int64_t key_factor_elems;        /* elements of the concatenated R_g blocks */

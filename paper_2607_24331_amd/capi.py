@@ -62,6 +62,7 @@ class PlanGeometry(ctypes.Structure):
         ("decode_waves", ctypes.c_int32),
         ("decode_ring", ctypes.c_int32),
         ("value_tiles_per_wave", ctypes.c_int32),
+        ("key_chunk_loads", ctypes.c_int32),
         ("page_elems", ctypes.c_int64),
         ("value_base", ctypes.c_int64),
         ("key_factor_elems", ctypes.c_int64),

@@ -104,11 +104,13 @@ __global__ __launch_bounds__(64) void fold_blocks(const float* __restrict__ q,
   const int j = blockIdx.y, pr = blockIdx.z;           // (sequence, slice) on x: grid x is wide
   const int J = mt.n_slices;
   const int b = blockIdx.x / J, slice = blockIdx.x % J;
-  const int nch0 = mt.kc1[slice][0] - mt.kc0[slice][0];
-  const int npairs = nch0 + (mt.nt > 1 ? mt.kc1[slice][1] - mt.kc0[slice][1] : 0);
+  const int nch0 = mt.kln[slice][0][0] + mt.kln[slice][0][1];
+  const int npairs = nch0 + (mt.nt > 1 ? mt.kln[slice][1][0] + mt.kln[slice][1][1] : 0);
   if (pr >= npairs) return;
   const int n = pr < nch0 ? 0 : 1;
-  const int c = mt.kc0[slice][n] + pr - (n ? nch0 : 0);
+  const int ci = pr - (n ? nch0 : 0);                   // position in the tile's chunk list
+  const int c = ci < mt.kln[slice][n][0] ? mt.kst[slice][n][0] + ci
+                                         : mt.kst[slice][n][1] + (ci - mt.kln[slice][n][0]);
   const int row = mt.hord[slice][16 * n + j];           // query i * H_q + head h, or -1
   const int h = row < 0 ? -1 : row % tb.n_q_heads, qi = row < 0 ? 0 : row / tb.n_q_heads;
   const int lane = threadIdx.x, kk = lane & 31, half = lane >> 5;
@@ -184,8 +186,8 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
   const int np = (t1 - t0 + 63) / 64;
 
   // ---- LDS carve-up
-  const int nch0 = mt.kc1[slice][0] - mt.kc0[slice][0];
-  const int npairs = nch0 + (NT > 1 ? mt.kc1[slice][1] - mt.kc0[slice][1] : 0);
+  const int nch0 = mt.kln[slice][0][0] + mt.kln[slice][0][1];
+  const int npairs = nch0 + (NT > 1 ? mt.kln[slice][1][0] + mt.kln[slice][1][1] : 0);
   u32x4* qblk = reinterpret_cast<u32x4*>(smem);                         // [npairs][2][64]
   bf16* p_lds = reinterpret_cast<bf16*>(smem + size_t(npairs) * 2048);  // [32][kPStride]
   float* red_max = reinterpret_cast<float*>(p_lds + 32 * kPStride);     // [8][32]
@@ -201,14 +203,22 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
   const bool scoring = w < SW;
   const int n_w = scoring ? (w * MPW) / 4 : 0;        // score N-tile
   const int mb_w = scoring ? (w * MPW) % 4 : 0;       // first score M-tile
-  const int kc0_w = mt.kc0[slice][n_w];
-  const int nch_w = mt.kc1[slice][n_w] - kc0_w;
+  // the tile's key chunks: list position ci is chunk st0_w + ci below
+  // ln0_w, else st1_w + (ci - ln0_w)
+  const int st0_w = mt.kst[slice][n_w][0], ln0_w = mt.kln[slice][n_w][0];
+  const int st1_w = mt.kst[slice][n_w][1];
+  const int nch_w = ln0_w + mt.kln[slice][n_w][1];
   const int nk_real = scoring ? nch_w * MPW : 0;      // key items a page
   const int NK = (nk_real + RING - 1) / RING * RING;  // padded to whole ring blocks
   const int pair0_w = (n_w == 0) ? 0 : nch0;
   const int mt0_w = w * mt.mtw;
   const int mcnt_w = max(0, min(mt.mtw, mt.mt_v - mt0_w));
-  const int kc_last = mt.kc1[slice][n_w] - 1;
+  // only the last chunk of the key latent can hold columns beyond r; its
+  // list position in this tile, or -1
+  const int kc_last = (RK - 1) / 32;
+  const int ci_last = (kc_last >= st0_w && kc_last < st0_w + ln0_w) ? kc_last - st0_w
+                    : (kc_last >= st1_w && kc_last < st1_w + nch_w - ln0_w) ? ln0_w + kc_last - st1_w
+                    : -1;
   // causal limit of this lane's score column: query i of Q sits at position
   // T_b - Q + i and sees the positions before it and its own
   int lim = T_b;
@@ -245,7 +255,7 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
     // key chunk c holds the 64 slots contiguously (2048 elements); M-tile m
     // of it is the 512-element run starting at m * 512.  Value tile u (16
     // ranks) holds the two 32-token halves as 512-element runs from u * 1024.
-    r.base = r.kind == 0 ? 2 * (2048 * (kc0_w + r.idx0 / MPW) + 512 * mb_w)
+    r.base = r.kind == 0 ? 2 * (512 * mb_w)
                          : 2 * (int(value_base) + 1024 * (mt0_w + (r.idx0 - NK) / 2));
     return r;
   };
@@ -254,8 +264,9 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
     int off = kOutOfRange;
     if (pb.kind == 0) {
       const int i = pb.idx0 + s;
-      const int c = kc0_w + i / MPW;
-      const int o = pb.base + 2 * (512 * (s % MPW) + 2048 * (s / MPW)) + lane_key;
+      const int ci = i / MPW;
+      const int c = ci < ln0_w ? st0_w + ci : st1_w + (ci - ln0_w);
+      const int o = pb.base + 2 * (512 * (s % MPW) + 2048 * c) + lane_key;
       const bool ok = (i < nk_real) & (32 * c + 8 * lq < RK);     // no short-circuit branches
       off = ok ? o : kOutOfRange;
     } else if (pb.kind == 1) {
@@ -329,7 +340,7 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
           blo = qblk[(pr * 2 + 1) * 64 + lane];
         }
         u32x4 a = ring[s];
-        if (kc0_w + c == kc_last) a = keep_first(a, kvalid_last);
+        if (c == ci_last) a = keep_first(a, kvalid_last);
         S[s % MPW] = mfma(a, bhi, S[s % MPW]);
         S[s % MPW] = mfma(a, blo, S[s % MPW]);
         ring[s] = issue(pbk, s);

@@ -31,11 +31,13 @@ struct HeadTables {
 constexpr int kMaxSlices = 8;     // (query, head) row slices of the MFMA decode path
 constexpr int kSliceHeads = 32;   // at most two 16-head MFMA tiles per slice
 
-// Schedule of the MFMA decode path (bf16 latents), fixed by the plan.  Query
-// heads are ordered by (group, head) and cut into J slices of at most 32;
-// a work-group serves one slice of one context split, so each group's key
-// columns form one contiguous range and, with J = 1, every latent byte is
-// read by exactly one work-group.
+// Schedule of the MFMA decode path (bf16 latents), fixed by the plan.  Rows
+// (query, head) are ordered by (group, head, query), with the groups taken
+// in the order the plan finds cheapest, and cut into J slices of at most
+// 32; a work-group serves one slice of one context split.  The key columns
+// a 16-row tile needs are the union of its groups' columns: at most two
+// ranges of 32-column chunks, (kst[.][.][0], kln[.][.][0]) then
+// (kst[.][.][1], kln[.][.][1]).
 struct MfmaTables {
   int32_t n_slices;                        // J
   int32_t q_heads;                         // H_q
@@ -49,8 +51,8 @@ struct MfmaTables {
   int32_t max_pairs;                       // most LDS query blocks of any slice
   int32_t slice_heads[kMaxSlices];         // real rows in slice s
   int32_t hord[kMaxSlices][kSliceHeads];   // slot -> row i * H_q + h (query i, head h), -1 padding
-  int32_t kc0[kMaxSlices][2];              // first 32-column key chunk of (slice, tile)
-  int32_t kc1[kMaxSlices][2];              // one past the last
+  int32_t kst[kMaxSlices][2][2];           // first key chunk of each range of (slice, tile)
+  int32_t kln[kMaxSlices][2][2];           // chunks in each range (0 for an unused range)
 };
 
 // Launch shape of one decode call, fixed by the plan and (batch, max_context).
@@ -89,6 +91,7 @@ struct dckv_plan {
   dckv::HeadTables tables;
   bool mfma_ok = false;              // bf16 MFMA decode path applies
   dckv::MfmaTables mfma{};
+  int32_t key_chunk_loads = 0;       // key chunks the MFMA tiles load a page
   hipEvent_t prof_before = nullptr;  // benchmark instrumentation of the split kernel
   hipEvent_t prof_after = nullptr;
 };

@@ -31,25 +31,80 @@ bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p
 
 namespace dckv {
 
+namespace {
+
+// Places the rows of the groups, taken in the order `gorder`, into the J
+// slices of `t` and records the key-chunk ranges of every 16-row tile.
+// Returns false when some tile's chunks do not fit in two ranges.
+bool place_rows(const dckv_plan& p, const std::vector<std::vector<int32_t>>& rows_of,
+                const std::vector<int32_t>& gorder, int32_t J, int32_t per, MfmaTables& t,
+                int32_t* total_chunks) {
+  std::vector<int32_t> order;
+  order.reserve(size_t(p.Q) * p.Hq);
+  for (int32_t g : gorder) order.insert(order.end(), rows_of[g].begin(), rows_of[g].end());
+  const int32_t nrows = int32_t(order.size());
+  const int32_t nchunks = (p.RK + 31) / 32;
+  int32_t max_pairs = 0, total = 0;
+  std::vector<char> used(nchunks);
+  for (int32_t s = 0; s < J; ++s) {
+    const int32_t h0 = std::min(nrows, s * per), h1 = std::min(nrows, (s + 1) * per);
+    t.slice_heads[s] = h1 - h0;
+    for (int32_t i = 0; i < kSliceHeads; ++i) t.hord[s][i] = (h0 + i < h1) ? order[h0 + i] : -1;
+    int32_t pairs = 0;
+    for (int32_t n = 0; n < 2; ++n) {
+      t.kst[s][n][0] = t.kst[s][n][1] = 0;
+      t.kln[s][n][0] = t.kln[s][n][1] = 0;
+      if (n >= t.nt) continue;
+      std::fill(used.begin(), used.end(), 0);
+      for (int32_t i = 16 * n; i < 16 * n + 16; ++i) {
+        const int32_t row = t.hord[s][i];
+        if (row < 0) continue;
+        const int32_t g = p.group_of_kv[(row % p.Hq) / p.qpk];
+        for (int32_t c = p.koff[g] / 32; c < (p.koff[g] + p.ranks[g] + 31) / 32; ++c) used[c] = 1;
+      }
+      int32_t nr = 0;
+      for (int32_t c = 0; c < nchunks; ++c) {
+        if (!used[c] || (c > 0 && used[c - 1])) continue;
+        if (nr == 2) return false;
+        int32_t e = c;
+        while (e < nchunks && used[e]) ++e;
+        t.kst[s][n][nr] = c;
+        t.kln[s][n][nr] = e - c;
+        ++nr;
+      }
+      pairs += t.kln[s][n][0] + t.kln[s][n][1];
+    }
+    max_pairs = std::max(max_pairs, pairs);
+    total += pairs;
+  }
+  t.max_pairs = max_pairs;
+  *total_chunks = total;
+  return true;
+}
+
+// Items the slowest wave loads a page (key items padded to whole rings,
+// then the value items, also padded): the pace between the two softmax
+// barriers of a page.
+int32_t padded_items(const MfmaTables& t, int32_t ring) {
+  const int32_t sw = std::min(4 * t.nt, t.waves), mpw = 4 * t.nt / sw;
+  int32_t nk_max = 0;
+  for (int32_t s = 0; s < t.n_slices; ++s)
+    for (int32_t n = 0; n < t.nt; ++n) {
+      const int32_t nk = (t.kln[s][n][0] + t.kln[s][n][1]) * mpw;
+      nk_max = std::max(nk_max, (nk + ring - 1) / ring * ring);
+    }
+  return nk_max + (2 * t.mtw_t + ring - 1) / ring * ring;
+}
+
+}  // namespace
+
 void build_mfma_tables(dckv_plan& p) {
   p.mfma_ok = false;
   p.mfma = MfmaTables{};
   if (p.dtype != DCKV_BF16) return;
   if (p.dh % 8 != 0) return;                   // the up-projection reads 8 columns at a time
   MfmaTables& t = p.mfma;
-  // Rows (query i, head h), numbered i * H_q + h, ordered by (group of the
-  // KV head, head, query): the rows of one group are adjacent, so a tile's
-  // key columns are one range, and the queries of one head share a tile.
   const int32_t nrows = p.Q * p.Hq;
-  std::vector<int32_t> order(nrows);
-  for (int32_t r = 0; r < nrows; ++r) order[r] = r;
-  std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
-    const int32_t ha = a % p.Hq, hb = b % p.Hq;
-    const int32_t ga = p.group_of_kv[ha / p.qpk], gb = p.group_of_kv[hb / p.qpk];
-    if (ga != gb) return ga < gb;
-    if (ha != hb) return ha < hb;
-    return a < b;
-  });
   int32_t J = p.head_slices > 0 ? p.head_slices : (nrows + kSliceHeads - 1) / kSliceHeads;
   if (J > kMaxSlices || J > nrows) return;
   const int32_t per = (nrows + J - 1) / J;
@@ -58,32 +113,6 @@ void build_mfma_tables(dckv_plan& p) {
   t.q_heads = p.Hq;
   t.queries = p.Q;
   t.nt = (per + 15) / 16;
-  int32_t max_pairs = 0;
-  for (int32_t s = 0; s < J; ++s) {
-    const int32_t h0 = std::min(nrows, s * per), h1 = std::min(nrows, (s + 1) * per);
-    t.slice_heads[s] = h1 - h0;
-    for (int32_t i = 0; i < kSliceHeads; ++i) t.hord[s][i] = (h0 + i < h1) ? order[h0 + i] : -1;
-    int32_t pairs = 0;
-    for (int32_t n = 0; n < t.nt; ++n) {
-      int32_t lo = p.RK, hi = 0;
-      for (int32_t i = 16 * n; i < 16 * n + 16; ++i) {
-        const int32_t row = t.hord[s][i];
-        if (row < 0) continue;
-        const int32_t g = p.group_of_kv[(row % p.Hq) / p.qpk];
-        lo = std::min(lo, p.koff[g]);
-        hi = std::max(hi, p.koff[g] + p.ranks[g]);
-      }
-      if (hi <= lo) {
-        t.kc0[s][n] = t.kc1[s][n] = 0;
-        continue;
-      }
-      t.kc0[s][n] = lo / 32;
-      t.kc1[s][n] = (hi + 31) / 32;
-      pairs += t.kc1[s][n] - t.kc0[s][n];
-    }
-    max_pairs = std::max(max_pairs, pairs);
-  }
-  t.max_pairs = max_pairs;
   t.mt_v = (p.rv + 15) / 16;
   // Eight waves (two a SIMD, so one wave's loads overlap the other's MFMAs)
   // whenever every wave gets at least one 16-rank value tile; four waves
@@ -98,29 +127,39 @@ void build_mfma_tables(dckv_plan& p) {
       break;
     }
   if (t.mtw_t == 0) return;
-  // Ring depth: every wave's key items and the value items of a page are
-  // padded to whole rings, and the slowest wave sets the pace between the
-  // two softmax barriers of a page, so take the depth with the fewest
-  // padded items for the slowest wave (the deeper ring on a tie).
-  {
-    const int32_t sw = std::min(4 * t.nt, t.waves), mpw = 4 * t.nt / sw;
-    int32_t best = 0, best_cost = 0;
+
+  // Rows of each group in (head, query) order: row i * H_q + h.
+  std::vector<std::vector<int32_t>> rows_of(p.G);
+  for (int32_t h = 0; h < p.Hq; ++h)
+    for (int32_t i = 0; i < p.Q; ++i) rows_of[p.group_of_kv[h / p.qpk]].push_back(i * p.Hq + h);
+
+  // Group order and ring depth: the slowest wave's padded items a page
+  // first, then the key chunks loaded by all tiles (a group cut by a tile
+  // boundary is loaded by both tiles); ties keep the earlier candidate, so
+  // the group-id order and the deeper ring win.  Every order is tried for
+  // up to seven groups; beyond that the group-id order alone.
+  std::vector<int32_t> gorder(p.G);
+  for (int32_t g = 0; g < p.G; ++g) gorder[g] = g;
+  const bool search = p.G <= 7;
+  MfmaTables cand = t, best = t;
+  int32_t best_cost = -1, best_total = 0;
+  do {
+    int32_t total = 0;
+    if (!place_rows(p, rows_of, gorder, J, per, cand, &total)) continue;
     for (int32_t ring : {16, 12}) {
-      int32_t nk_max = 0;
-      for (int32_t s = 0; s < J; ++s)
-        for (int32_t n = 0; n < t.nt; ++n) {
-          const int32_t nk = (t.kc1[s][n] - t.kc0[s][n]) * mpw;
-          nk_max = std::max(nk_max, (nk + ring - 1) / ring * ring);
-        }
-      const int32_t cost = nk_max + (2 * t.mtw_t + ring - 1) / ring * ring;
-      if (best == 0 || cost < best_cost) {
-        best = ring;
+      const int32_t cost = padded_items(cand, ring);
+      if (best_cost < 0 || cost < best_cost || (cost == best_cost && total < best_total)) {
+        best = cand;
+        best.ring = ring;
         best_cost = cost;
+        best_total = total;
       }
     }
-    t.ring = best;
-  }
-  const int64_t lds = int64_t(max_pairs) * 2048 + 32 * 72 * 2 + 2 * 8 * 32 * 4 + 256 * 4;
+  } while (search && std::next_permutation(gorder.begin(), gorder.end()));
+  if (best_cost < 0) return;                    // unreachable: the group-id order has one range a tile
+  t = best;
+  p.key_chunk_loads = best_total;
+  const int64_t lds = int64_t(t.max_pairs) * 2048 + 32 * 72 * 2 + 2 * 8 * 32 * 4 + 256 * 4;
   if (lds > 160 * 1024) return;
   p.mfma_ok = true;
 }
@@ -282,6 +321,7 @@ int dckv_plan_info(const dckv_plan* p, dckv_plan_geometry* geo, int32_t* koff,
     geo->decode_waves = p->mfma_ok ? p->mfma.waves : 0;
     geo->decode_ring = p->mfma_ok ? p->mfma.ring : 0;
     geo->value_tiles_per_wave = p->mfma_ok ? p->mfma.mtw : 0;
+    geo->key_chunk_loads = p->mfma_ok ? p->key_chunk_loads : 0;
     geo->page_elems = p->page_elems;
     geo->value_base = p->value_base;
     geo->key_factor_elems = p->key_factor_elems;

@@ -70,6 +70,11 @@ SMALL = {
     "valu_bf16": dict(hidden=2560, num_q_heads=32, num_kv_heads=32, head_dim=128,
                       sizes=(8, 8, 8, 8), group_rank=(300, 200, 100, 50), value_rank=2304,
                       seq_lens=(200, 70), permute_pages=False, split=128),
+    # groups of 8, 12 and 12 rows: the plan cuts the smallest group, so one
+    # 16-row tile loads two separate ranges of key chunks
+    "gqa_reordered": dict(hidden=512, num_q_heads=32, num_kv_heads=8, head_dim=64, sizes=(2, 3, 3),
+                          group_rank=(96, 128, 160), value_rank=256, seq_lens=(900, 300, 65),
+                          permute_pages=True, split=256),
 }
 
 
@@ -136,7 +141,7 @@ def test_small_decode_all_rows(name):
 # value-tile capacities 6, 8 and 32 -- each checked on every row
 LAUNCH_SHAPES = [("gqa_uneven", 4, 0), ("gqa_uneven", 8, 2), ("singletons", 4, 0),
                  ("mha32_two_tiles", 4, 0), ("mha32_two_tiles", 4, 2), ("valu_bf16", 8, 2),
-                 ("single_group", 4, 0)]
+                 ("single_group", 4, 0), ("gqa_reordered", 4, 0)]
 
 
 @pytest.mark.parametrize("name, waves, slices", LAUNCH_SHAPES)

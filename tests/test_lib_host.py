@@ -195,3 +195,24 @@ def test_queries_per_seq_plan():
     assert four.workspace_bytes(1, 131072) > one.workspace_bytes(1, 131072)
     # 32 heads x 16 queries = 512 rows exceed the eight slices: portable path
     assert Plan(*args, queries_per_seq=16).geometry["mfma_path"] == 0
+
+
+def test_group_order_cuts_the_smallest_group():
+    from paper_2607_24331_amd import Plan
+    # 32 query heads over 8 KV heads (4 each); groups of 2, 3 and 3 KV heads
+    # (8, 12 and 12 rows) with ranks 96, 128, 160: key chunks 0-2, 3-6, 7-11.
+    # Two 16-row tiles must cut one group; in group-id order that is group 1
+    # (tiles load chunks 0-6 and 3-11: 16 loads), while cutting group 0
+    # (tiles {g1 + 4 rows of g0}, {4 rows of g0 + g2}) loads 7 + 8 = 15.
+    p = Plan(512, 32, 8, 64, [0, 0, 1, 1, 1, 2, 2, 2], [96, 128, 160], 256, "bf16")
+    assert p.geometry["mfma_path"] == 1 and p.geometry["key_chunk_loads"] == 15
+    # every group whole in one tile: each chunk loaded once
+    p = Plan(512, 32, 8, 64, [0, 0, 0, 0, 1, 1, 1, 1], [96, 128], 256, "bf16")
+    assert p.geometry["key_chunk_loads"] == 7
+    # the GQA decode workload: groups of 8, 12 and 12 rows with 6, 8 and 10
+    # chunks; cutting the 6-chunk group loads 30 chunks, and with 16 and 14
+    # chunks a tile the 16-deep ring pads no key item
+    g = _plan(make_workload("gqa8b_b4_t32k")).geometry
+    assert g["key_chunk_loads"] == 30 and g["decode_ring"] == 16
+    # the portable path reports none
+    assert _plan(make_workload("tiny_mha_f32")).geometry["key_chunk_loads"] == 0
