@@ -37,6 +37,7 @@ constexpr int kRing = 16;                 // loads in flight per wave
 constexpr int kPageSlots = 256;           // pages per split the LDS page list holds
 constexpr int kPStride = 72;              // bf16 per head row of the p tile (64 + pad)
 constexpr int kMergeRanks = 8;            // value ranks per merge work-group
+constexpr int kQblkLoads = 16;            // folded-query loads a thread issued at the split's start
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -174,16 +175,10 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
   const int u = grp * 8 + (rr % 8);       // all slices of unit u share an XCD (ids equal mod 8)
   if (u >= n_units) return;               // n_units = batch * n_split (the grid is padded)
   const int b = u / n_split, split = u % n_split;
-  int T_b = seq_lens[b];
-  T_b = T_b < 0 ? 0 : (T_b > max_context ? max_context : T_b);
-  const int t0 = split * split_tokens;
-  const int t1 = min(t0 + split_tokens, T_b);
-  if (t0 >= t1) return;                   // the merge only reads splits holding tokens
-
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, provably uniform
   const int lr = lane & 15, lq = lane >> 4;
-  const int np = (t1 - t0 + 63) / 64;
+  const int t0 = split * split_tokens;
 
   // ---- LDS carve-up
   const int nch0 = mt.kln[slice][0][0] + mt.kln[slice][0][1];
@@ -194,10 +189,33 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
   float* red_sum = red_max + 8 * 32;                                    // [8][32]
   int* pids = reinterpret_cast<int*>(red_sum + 8 * 32);                 // [kPageSlots]
 
-  for (int i = tid; i < np; i += W * 64) {
-    const int pg = page_table[int64_t(b) * max_pages + (t0 >> 6) + i];
-    pids[i] = (pg >= 0 && pg < num_pages) ? pg : -1;
-  }
+  // ---- the prologue's loads go out together, none waiting on another:
+  // this lane's query row (for the causal limit) and page-table entry, the
+  // folded-query blocks (built by fold_blocks) into registers, then the
+  // first page's table entry and the context length (scalar).  The vector
+  // loads are issued in the order they are consumed, so each wait leaves
+  // the later loads in flight.
+  // (every load is unconditional at a clamped, valid address, so no branch
+  // hides a load from the wait counting; unused values are dropped)
+  constexpr int SWc = (4 * NT < W) ? 4 * NT : W;
+  const int hrow_raw = mt.hord[slice][min(16 * ((min(w, SWc - 1) * ((4 * NT) / SWc)) / 4) + lr, kSliceHeads - 1)];
+  const int hrow = w < SWc ? hrow_raw : -1;
+  const int pg_lane = page_table[int64_t(b) * max_pages + min((t0 >> 6) + tid, max_pages - 1)];
+  const u32x4* qsrc = qblk_ws + int64_t(b * J + slice) * mt.max_pairs * 128;
+  const int n16 = npairs * 128;
+  u32x4 qv[kQblkLoads];
+#pragma unroll
+  for (int k = 0; k < kQblkLoads; ++k) qv[k] = qsrc[min(tid + k * W * 64, n16 - 1)];
+  int pid0 = (t0 >> 6) < max_pages ? page_table[int64_t(b) * max_pages + (t0 >> 6)] : -1;
+  pid0 = __builtin_amdgcn_readfirstlane((pid0 >= 0 && pid0 < num_pages) ? pid0 : -1);
+  int T_b = seq_lens[b];
+  T_b = T_b < 0 ? 0 : (T_b > max_context ? max_context : T_b);
+  const int t1 = min(t0 + split_tokens, T_b);
+  if (t0 >= t1) return;                   // the merge only reads splits holding tokens
+  const int np = (t1 - t0 + 63) / 64;
+
+  static_assert(kPageSlots <= W * 64, "one page-table entry a thread");
+  if (tid < np) pids[tid] = (pg_lane >= 0 && pg_lane < num_pages) ? pg_lane : -1;
 
   // ---- wave roles
   const bool scoring = w < SW;
@@ -222,10 +240,7 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
   // causal limit of this lane's score column: query i of Q sits at position
   // T_b - Q + i and sees the positions before it and its own
   int lim = T_b;
-  if (scoring) {
-    const int row = mt.hord[slice][16 * n_w + lr];
-    if (row >= 0) lim = T_b - mt.queries + row / mt.q_heads + 1;
-  }
+  if (scoring && hrow >= 0) lim = T_b - mt.queries + hrow / mt.q_heads + 1;
   const int kvalid_last = min(8, max(0, RK - (32 * kc_last + 8 * lq)));
 
   // ---- producer.  The item stream of a page is NK key items (chunk-major,
@@ -239,13 +254,15 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
   const int page_bytes = int(page_elems * 2);
   const int blocks_pp = (NK + NV) / RING;             // producer blocks a page
   int prod_block = 0;                                 // producer block counter over the split
-  __syncthreads();                                    // pids ready
-  auto setup = [&](int pblk) {
+  // the first block (page 0) takes its page from pid0: the LDS page list is
+  // read only after the prologue's barrier
+  auto setup = [&](int pblk, bool first = false) {
     ProdBlock r;
     const int page = pblk / blocks_pp;
     const int blk = pblk - page * blocks_pp;
     int pid = -1;
-    if (page < np) pid = __builtin_amdgcn_readfirstlane(pids[page]);
+    if (first) pid = pid0;
+    else if (page < np) pid = __builtin_amdgcn_readfirstlane(pids[page]);
     const bf16* base = pid >= 0 ? pool + int64_t(pid) * page_elems : pool;
     r.rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(base), 0,
                                                pid >= 0 ? page_bytes : 0, kRsrcWord3);
@@ -280,23 +297,27 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
 
   u32x4 ring[RING];
   {
-    const ProdBlock pb0 = setup(prod_block++);
+    const ProdBlock pb0 = setup(prod_block++, true);
 #pragma unroll
     for (int s = 0; s < RING; ++s) ring[s] = issue(pb0, s);
   }
 
-  // ---- block-diagonal folded query (hi/lo bf16 MFMA B operands, built by
-  // fold_blocks): a straight 16-byte copy into LDS, eight loads in flight
-  // a thread, behind the ring's first loads.
+  // ---- block-diagonal folded query (hi/lo bf16 MFMA B operands): the
+  // registers loaded above go to LDS (their loads precede the ring's, so
+  // the ring stays in flight); a plan with more blocks than the registers
+  // hold copies the rest here, eight loads in flight a thread.
+#pragma unroll
+  for (int k = 0; k < kQblkLoads; ++k) {
+    const int idx = tid + k * W * 64;
+    if (idx < n16) qblk[idx] = qv[k];
+  }
   {
-    const u32x4* src = qblk_ws + int64_t(b * J + slice) * mt.max_pairs * 128;
-    const int n16 = npairs * 128;
-    for (int base = tid; base < n16; base += 8 * W * 64) {
+    for (int base = tid + kQblkLoads * W * 64; base < n16; base += 8 * W * 64) {
       u32x4 v[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
         const int idx = base + k * W * 64;
-        if (idx < n16) v[k] = src[idx];
+        if (idx < n16) v[k] = qsrc[idx];
       }
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
