@@ -16,10 +16,18 @@ Modules
   attention   decode: rebuild K = Z_g R_g and V = Z_v R_v per head
               (Sec. III-A, III-C, III-D), then textbook two-pass softmax
               attention in fp64
+  dense       uncompressed paged K/V decode (the comparison baseline)
+  compress    offline key compression, Algorithm 1: CKA head similarity,
+              agglomerative clustering, energy ranks, greedy budget
+              adjustment, per-group SVD, the cluster-count objective
+              (Sec. III-A, III-C)
+  calibrate   value calibration refinement: calibration error and the two
+              closed-form factor updates (Sec. III-D)
 
 Parity status: every function here is pinned by the `-m "not gpu"` tests
 (closed forms, full-rank equivalence with uncompressed attention computed by
 a library routine, printed Table 1 figures, exhaustive/brute-force checks).
 """
 
-from . import bf16, bookkeeping, params, layout, append, attention  # noqa: F401
+from . import bf16, bookkeeping, params, layout, append, attention, dense  # noqa: F401
+from . import compress, calibrate  # noqa: F401
