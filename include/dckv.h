@@ -249,6 +249,61 @@ int dckv_dense_decode(int32_t num_q_heads, int32_t num_kv_heads, int32_t head_di
                       size_t workspace_bytes, void* before_event, void* after_event,
                       void* stream);
 
+/* ------------------------------------------------------------------------
+ * Offline compression: run once per layer before serving, never on the
+ * decode path.
+ *
+ * Gram matrix of samples (Sec. III-A: linear CKA compares centred
+ * representations; Sec. III-D: the calibration Gram X^T X):
+ *   G = A~^T A~, with A~ = A - 1 mu^T (mu: the column means) when center is
+ *   nonzero, else A~ = A.
+ *   A          device [rows, cols] row-major, dtype DCKV_F32 or DCKV_BF16,
+ *              16-byte aligned; 1 <= rows <= 65535*256, cols a multiple of 8
+ *              in [8, 32768]
+ *   G          device [cols, cols] fp32, written in full (both triangles)
+ *   workspace  device, at least dckv_gram_workspace_bytes (may be NULL
+ *              when that is 0), 256-byte aligned
+ * Products and sums are fp32 (MFMA f32) in a fixed order: bitwise
+ * reproducible.  Errors: DCKV_EINVAL (shape, null pointer), DCKV_EDTYPE,
+ * DCKV_EALIGN, DCKV_EWORKSPACE, DCKV_EHIP; nothing is launched on error. */
+int dckv_gram_workspace_bytes(int64_t rows, int32_t cols, int32_t center, size_t* bytes);
+int dckv_gram(const void* A, int32_t dtype, int64_t rows, int32_t cols, int32_t center, float* G,
+              void* workspace, size_t workspace_bytes, void* stream);
+
+/* Head similarity (Sec. III-C) from a centred Gram of the heads'
+ * activations (columns h*d_h .. h*d_h + d_h - 1 belong to head h):
+ *   S[i][j] = ||G_ij||_F^2 / (||G_ii||_F ||G_jj||_F), G_ij the d_h x d_h block
+ *   of heads i and j -- the linear CKA of Sec. III-A; 0 where a head's block
+ *   is zero.
+ *   G device [h*d_h, h*d_h] fp32; S device [h, h] fp32 (out).
+ * 1 <= h <= DCKV_MAX_HEADS, 1 <= d_h <= DCKV_MAX_HEAD_DIM.  Fixed-order sums. */
+int dckv_head_similarity(const float* G, int32_t num_heads, int32_t head_dim, float* S,
+                         void* stream);
+
+/* Host: Algorithm 1's head clustering (ClusterHeads, Sec. III-C):
+ * agglomerative clustering into K groups with average linkage on the
+ * distance 1 - S[i][j]; on equal distances the pair of clusters whose
+ * smallest head ids are lexicographically smallest merges first.  Groups
+ * are numbered in order of their smallest head.
+ *   S host [h][h] double (symmetric); group_of_head host [h] (out).
+ * 1 <= K <= h <= DCKV_MAX_HEADS.  Makes no HIP call. */
+int dckv_cluster_heads(const double* S, int32_t num_heads, int32_t K, int32_t* group_of_head);
+
+/* Host: Algorithm 1's rank allocation (InitRanksByEnergy then GreedyAdjust,
+ * Sec. III-C) for K groups of a key projection with rank budget r:
+ *   init_ranks[i] = floor(r * energy[i] / energy_total + 1/2), clipped to
+ *   [1, rank_cap[i]]; then, while sum_i ranks[i]*heads[i] > 4 r (the budget
+ *   sum_i r_i alpha_i <= 4 r / h) or sum_i ranks[i] > r, lower by one the
+ *   rank with the smallest sigma_i[r_i - 1]^2 * h / heads[i] among ranks
+ *   above 1 (equal costs: the lower group id); h = sum of heads.
+ *   heads [K], energy [K] (||W_i||_F^2), rank_cap [K] (min(m, h_i d_h)),
+ *   sigma [K][sigma_stride] (singular values of W_i, descending, at least
+ *   rank_cap[i] of them) -- all host; init_ranks, ranks [K] host (out).
+ * Makes no HIP call. */
+int dckv_allocate_ranks(int32_t K, const int32_t* heads, const double* energy,
+                        double energy_total, const double* sigma, int32_t sigma_stride,
+                        const int32_t* rank_cap, int32_t r, int32_t* init_ranks, int32_t* ranks);
+
 /* Message of the last failing call on this thread ("" if none). */
 const char* dckv_last_error(void);
 

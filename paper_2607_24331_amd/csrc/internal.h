@@ -98,6 +98,17 @@ struct dckv_plan {
 
 namespace dckv {
 
+// Records a formatted message for dckv_last_error() and returns status.
+int fail(int status, const char* fmt, ...);
+bool aligned(const void* p, uintptr_t a);
+
+// Offline contractions (gram.hip).
+size_t gram_workspace_bytes(int64_t rows, int32_t cols);
+hipError_t launch_gram(const void* A, int32_t dtype, int64_t rows, int32_t cols, bool center,
+                       float* G, void* workspace, hipStream_t stream);
+hipError_t launch_head_similarity(const float* G, int32_t h, int32_t d, float* S,
+                                  hipStream_t stream);
+
 // Builds plan.mfma and sets plan.mfma_ok (host only, no HIP call).
 void build_mfma_tables(dckv_plan& p);
 

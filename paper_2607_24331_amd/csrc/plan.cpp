@@ -15,6 +15,10 @@ namespace {
 
 thread_local std::string g_last_error;
 
+}  // namespace
+
+namespace dckv {
+
 int fail(int status, const char* fmt, ...) {
   char buf[512];
   va_list ap;
@@ -27,7 +31,10 @@ int fail(int status, const char* fmt, ...) {
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
-}  // namespace
+}  // namespace dckv
+
+using dckv::aligned;
+using dckv::fail;
 
 namespace dckv {
 

@@ -254,3 +254,78 @@ def dense_decode(q: torch.Tensor, kv_pool: torch.Tensor, page_table: torch.Tenso
                                   int(max_context), po, pw, workspace.numel(), eb, ea,
                                   _stream_handle(stream)), "dense_decode")
     return out
+
+
+# ---------------------------------------------------------------- offline calls
+def gram_workspace_bytes(rows: int, cols: int, center: bool = True) -> int:
+    n = ctypes.c_size_t(0)
+    _check(_lib.dckv_gram_workspace_bytes(int(rows), int(cols), int(bool(center)), ctypes.byref(n)),
+           "gram_workspace_bytes")
+    return n.value
+
+
+def gram(A: torch.Tensor, center: bool = True, out: Optional[torch.Tensor] = None,
+         workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """G = A~^T A~ (fp32 [cols, cols]) for samples A [rows, cols] (fp32 or
+    bf16 on the GPU); A~ is A with its column means removed when `center`."""
+    if A.dim() != 2:
+        raise ValueError("A must be [rows, cols]")
+    rows, cols = A.shape
+    dt = {torch.float32: 0, torch.bfloat16: 1}.get(A.dtype)
+    if dt is None:
+        raise TypeError("A must be float32 or bfloat16")
+    pa = _dev(A, "A", A.dtype)
+    if out is None:
+        out = torch.empty((cols, cols), dtype=torch.float32, device=A.device)
+    po = _dev(out, "out", torch.float32, (cols, cols))
+    need = gram_workspace_bytes(rows, cols, center)
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=A.device)
+    pw = _dev(workspace, "workspace", torch.uint8) if workspace is not None else None
+    _check(_lib.dckv_gram(pa, dt, int(rows), int(cols), int(bool(center)), po, pw,
+                          workspace.numel() if workspace is not None else 0, _stream_handle(stream)),
+           "gram")
+    return out
+
+
+def head_similarity(G: torch.Tensor, num_heads: int, head_dim: int,
+                    out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """S [h, h] fp32 from a centred Gram G [h*d_h, h*d_h] of per-head activations."""
+    n = num_heads * head_dim
+    pg = _dev(G, "G", torch.float32, (n, n))
+    if out is None:
+        out = torch.empty((num_heads, num_heads), dtype=torch.float32, device=G.device)
+    ps = _dev(out, "out", torch.float32, (num_heads, num_heads))
+    _check(_lib.dckv_head_similarity(pg, int(num_heads), int(head_dim), ps, _stream_handle(stream)),
+           "head_similarity")
+    return out
+
+
+def cluster_heads(S, K: int):
+    """Group id of every head (host call): average-linkage clustering of 1 - S."""
+    import numpy as np
+    Sd = np.ascontiguousarray(np.asarray(S, dtype=np.float64))
+    h = Sd.shape[0]
+    if Sd.shape != (h, h):
+        raise ValueError("S must be square")
+    out = (ctypes.c_int32 * h)()
+    _check(_lib.dckv_cluster_heads(Sd.ctypes.data_as(ctypes.c_void_p), h, int(K), out), "cluster_heads")
+    return list(out)
+
+
+def allocate_ranks(heads: Sequence[int], energy: Sequence[float], energy_total: float,
+                   sigmas: Sequence, rank_cap: Sequence[int], r: int):
+    """(init_ranks, ranks) of the energy rule and the greedy budget step (host call)."""
+    import numpy as np
+    K = len(heads)
+    stride = max(len(s) for s in sigmas)
+    sig = np.zeros((K, stride))
+    for i, s in enumerate(sigmas):
+        sig[i, :len(s)] = np.asarray(s, dtype=np.float64)
+    en = np.ascontiguousarray(np.asarray(energy, dtype=np.float64))
+    init = (ctypes.c_int32 * K)()
+    ranks = (ctypes.c_int32 * K)()
+    _check(_lib.dckv_allocate_ranks(K, _i32_array(heads), en.ctypes.data_as(ctypes.c_void_p),
+                                    float(energy_total), sig.ctypes.data_as(ctypes.c_void_p), stride,
+                                    _i32_array(rank_cap), int(r), init, ranks), "allocate_ranks")
+    return list(init), list(ranks)
