@@ -87,7 +87,9 @@ def cluster_heads(S: np.ndarray, K: int) -> List[List[int]]:
         best = None
         for a in range(len(clusters)):
             for b in range(a + 1, len(clusters)):
-                d = np.mean([D[i, j] for i in clusters[a] for j in clusters[b]])
+                # mean over member pairs, summed in member order
+                d = sum(float(D[i, j]) for i in clusters[a] for j in clusters[b]) / (
+                    len(clusters[a]) * len(clusters[b]))
                 key = (d, min(clusters[a]), min(clusters[b]))
                 if best is None or key < best[0]:
                     best = (key, a, b)
@@ -146,7 +148,8 @@ def greedy_adjust(ranks: Sequence[int], sigmas: Sequence[np.ndarray], heads: Seq
         for i, (ri, hi) in enumerate(zip(ranks, heads)):
             if ri <= 1:
                 continue
-            cost = sigmas[i][ri - 1] ** 2 / (hi / h)      # Delta E_i / alpha_i
+            s = float(sigmas[i][ri - 1])
+            cost = s * s * h / hi                         # Delta E_i / alpha_i, alpha_i = h_i / h
             if best is None or cost < best[0]:
                 best = (cost, i)
         if best is None:                                  # every group is at rank 1
