@@ -53,7 +53,103 @@ def parse():
                          "kernel for scaling hardware traffic counters)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle sample")
+    ap.add_argument("--offline", choices=["cka", "calib"], default=None,
+                    help="time an offline compression contraction instead of the decode path: "
+                         "cka = centred Gram of 32 heads x 128 activations over 2048 samples plus "
+                         "the CKA head similarity; calib = calibration Gram X^T X, hidden 4096, "
+                         "8192 samples")
     return ap.parse_args()
+
+
+MFMA_F32_PEAK_TFLOPS = 157.3
+
+
+def main_offline(args, torch):
+    """Offline Gram contractions (fp32 MFMA) against the fp32 MFMA peak."""
+    import numpy as np
+    from paper_2607_24331_amd import gram, head_similarity
+    if args.offline == "cka":
+        h, d, N = 32, 128, 2048
+        cols, center = h * d, True
+        name = "cka_h32_d128_s2048"
+    else:
+        h = d = None
+        N, cols, center = 8192, 4096, False
+        name = "calib_m4096_s8192"
+    g = torch.Generator(device="cuda")
+    g.manual_seed(4242)
+    A = torch.randn((N, cols), generator=g, device="cuda") + 0.25
+    G = torch.empty((cols, cols), dtype=torch.float32, device="cuda")
+    S = torch.empty((h, h), dtype=torch.float32, device="cuda") if h else None
+
+    def step():
+        gram(A, center=center, out=G)
+        if h:
+            head_similarity(G, h, d, out=S)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    K = args.steps
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(K):
+        step()
+    t1.record()
+    torch.cuda.synchronize()
+    ms_step = t0.elapsed_time(t1) / K
+    # the Gram tile kernel alone: an uncentred launch is that one kernel
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    for a, b in ev:
+        a.record()
+        gram(A, center=False, out=G)
+        b.record()
+    torch.cuda.synchronize()
+    kern_ms = sum(a.elapsed_time(b) for a, b in ev) / K
+    flops = float(N) * cols * (cols + 1)          # the n(n+1)/2 distinct entries, 2 flops a term
+    rec = {
+        "metric": ("offline CKA head similarity: Gram TFLOP/s" if h
+                   else "offline calibration Gram TFLOP/s"),
+        "value": flops / (ms_step * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": K, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded N(0,1) + 0.25 samples)",
+        "config": {"workload": name, "samples": N, "cols": cols, "centred": center,
+                   "heads": h, "head_dim": d},
+        "roofline": {"kernel": "gram_tiles (fp32 MFMA)", "bound": "mfma",
+                     "achieved": flops / (kern_ms * 1e-3) / 1e12, "peak": MFMA_F32_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": flops / (kern_ms * 1e-3) / 1e12 / MFMA_F32_PEAK_TFLOPS,
+                     "traffic": None, "kernel_ms": kern_ms, "flops_per_launch": flops},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import calibrate as ocal
+        from oracle import compress as oc
+        An = A.double().cpu().numpy()
+        t = time.perf_counter()
+        if h:
+            oc.head_similarity(An, h, d)
+        else:
+            ocal.gram(An)
+        dt = time.perf_counter() - t
+        rec["cpu_baseline"] = {
+            "value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": _blas_threads(),
+            "kind": "oracle",
+            "sample": ("oracle head_similarity over the full input (fp64 numpy: per-pair CKA)"
+                       if h else "oracle gram over the full input (fp64 numpy X^T X)"),
+            "seconds": dt}
+    print(json.dumps(rec), flush=True)
+
+
+def _blas_threads():
+    """Threads of the BLAS numpy calls into (the oracle's matrix products)."""
+    try:
+        import numpy  # noqa: F401  (loads the BLAS)
+        from threadpoolctl import threadpool_info
+        return max([i.get("num_threads", 1) for i in threadpool_info()
+                    if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        return len(os.sched_getaffinity(0))
 
 
 def device_inputs(wl, plan, torch, Q=1):
@@ -327,6 +423,8 @@ def main():
     from paper_2607_24331_amd import Plan, decode, latent_append
     from workloads import make_workload
 
+    if args.offline:
+        return main_offline(args, torch)
     wl = make_workload(args.workload)
     if args.dense:
         return main_dense(args, torch, wl)

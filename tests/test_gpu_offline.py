@@ -26,10 +26,11 @@ def _gram_bound(A64, center, rows):
 
 # (rows, cols, dtype, centre): ragged sample counts (not a multiple of the
 # 32-sample step), column counts that leave partial 128-column tiles, one
-# sample, the smallest width
+# sample, the smallest width; 4000 columns take the 192-column tiles (the
+# last one partial)
 CASES = [(200, 72, "f32", True), (1000, 264, "f32", True), (1000, 264, "f32", False),
          (37, 8, "f32", True), (513, 392, "bf16", True), (1, 16, "f32", True),
-         (2048, 256, "bf16", False)]
+         (2048, 256, "bf16", False), (100, 4000, "f32", True), (70, 4000, "bf16", False)]
 
 
 @pytest.mark.parametrize("rows, cols, dtype, center", CASES)
