@@ -125,9 +125,11 @@ typedef struct dckv_plan_geometry {
   int32_t head_slices;             /* query-head slices of the MFMA path (0 otherwise) */
   int32_t queries_per_seq;         /* Q of the plan (at least 1) */
   int32_t decode_waves;            /* waves a decode work-group on the MFMA path (0 otherwise) */
-  int32_t decode_ring;             /* 16-byte loads in flight a wave on the MFMA path (12 or
-                                      16: the depth that pads the slowest wave's key and
-                                      value loads of a page least; 0 otherwise) */
+  int32_t decode_ring;             /* key-phase block of the MFMA path: 16-byte loads in
+                                      flight a wave while keys stream (12, 14 or 16: the
+                                      size that pads the slowest wave's key loads least;
+                                      value loads go in blocks of 12 or 16 fixed by the
+                                      value tiles a wave; 0 otherwise) */
   int32_t value_tiles_per_wave;    /* 16-rank value tiles a wave on the MFMA path (0 otherwise) */
   int32_t key_chunk_loads;         /* 32-column key chunks the MFMA path loads a 64-token page,
                                       summed over its 16-row tiles: a tile loads the chunks of

@@ -47,7 +47,7 @@ constexpr int kRsrcWord3 = 0x00020000;
 constexpr int kOutOfRange = 0x40000000;   // byte offset beyond any page
 constexpr int kNonTemporal = 2;           // cache policy of streamed latents: nt
 
-// One producer block: RING consecutive items of one page, all keys or all
+// One producer block: consecutive items of one page (KR keys or VR values),
 // values (kind 2: past the split, every load reads zero).
 struct ProdBlock {
   __amdgpu_buffer_rsrc_t rsrc;
@@ -153,8 +153,10 @@ __global__ __launch_bounds__(64) void fold_blocks(const float* __restrict__ q,
 
 // ---------------------------------------------------------------------------
 // W waves (4 or 8) a work-group; NT 16-head tiles; at most MTW value M-tiles
-// (16 ranks) a wave; RING loads in flight a wave.
-template <int W, int NT, int MTW, int RING>
+// (16 ranks) a wave; key ring blocks of KR loads, value ring blocks of VR
+// (12 or 16, whichever holds the 2 MTW value items of a page without
+// padding, or with the least).
+template <int W, int NT, int MTW, int KR>
 __global__ __launch_bounds__(W * 64, 1) void split_mfma(
     const u32x4* __restrict__ qblk_ws, const bf16* __restrict__ pool, int64_t num_pages,
     const int32_t* __restrict__ page_table, int max_pages, const int32_t* __restrict__ seq_lens,
@@ -164,8 +166,10 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
   constexpr int NH = 16 * NT;                          // head slots of the slice
   constexpr int SW = (4 * NT < W) ? 4 * NT : W;        // waves holding score tiles
   constexpr int MPW = (4 * NT) / SW;                   // score M-tiles (16 tokens) a scoring wave
-  constexpr int NV = ((2 * MTW + RING - 1) / RING) * RING;   // value items a page (padded)
-  static_assert(RING % 2 == 0 && RING % MPW == 0, "ring blocks hold whole chunks and k-steps");
+  constexpr int VR = ((2 * MTW) % 16 == 0) ? 16 : 12;  // value ring block
+  constexpr int RING = KR > VR ? KR : VR;              // ring slots
+  constexpr int NV = ((2 * MTW + VR - 1) / VR) * VR;   // value items a page (padded)
+  static_assert(KR % 2 == 0 && KR % MPW == 0 && VR % 2 == 0, "blocks hold whole chunks and k-steps");
   extern __shared__ __align__(16) unsigned char smem[];
 
   const int J = mt.n_slices;
@@ -227,7 +231,10 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
   const int st1_w = mt.kst[slice][n_w][1];
   const int nch_w = ln0_w + mt.kln[slice][n_w][1];
   const int nk_real = scoring ? nch_w * MPW : 0;      // key items a page
-  const int NK = (nk_real + RING - 1) / RING * RING;  // padded to whole ring blocks
+  // key items padded to whole blocks; with two block sizes every wave has at
+  // least one key block (all-dummy for a wave without score tiles), so the
+  // last key block's change of length is on every wave's schedule
+  const int NK = KR == VR ? (nk_real + KR - 1) / KR * KR : max(KR, (nk_real + KR - 1) / KR * KR);
   const int pair0_w = (n_w == 0) ? 0 : nch0;
   const int mt0_w = w * mt.mtw;
   const int mcnt_w = max(0, min(mt.mtw, mt.mt_v - mt0_w));
@@ -244,15 +251,20 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
   const int kvalid_last = min(8, max(0, RK - (32 * kc_last + 8 * lq)));
 
   // ---- producer.  The item stream of a page is NK key items (chunk-major,
-  // M-tile minor) then NV value items (M-tile-major, k-step minor).  The
-  // producer runs exactly one ring block ahead of the consumer and both
-  // lengths are whole blocks, so a producer block never spans two pages or
-  // two kinds: its page and kind are set once per block, and each issue is a
-  // single unconditional 16-byte buffer load (out-of-range offsets read 0).
+  // M-tile minor) in blocks of KR, then NV value items (M-tile-major, k-step
+  // minor) in blocks of VR.  The producer runs exactly one block ahead of the
+  // consumer: while block b is consumed, slot s of block b + 1 is issued as
+  // slot s of b is consumed; where b + 1 is longer, its extra slots (free,
+  // as b does not use them) are issued before b is consumed, and where it is
+  // shorter, b's last slots issue nothing.  Both lengths are whole blocks, so
+  // a producer block never spans two pages or two kinds: its page and kind
+  // are set once per block, and each issue is a single unconditional 16-byte
+  // buffer load (out-of-range offsets read 0).
   const int lane_key = 2 * (lr * 32 + 8 * lq);        // byte offsets of this lane
   const int lane_val = 2 * (lr * 32 + 8 * lq);
   const int page_bytes = int(page_elems * 2);
-  const int blocks_pp = (NK + NV) / RING;             // producer blocks a page
+  const int nkb = NK / KR;                            // key blocks a page
+  const int blocks_pp = nkb + NV / VR;                // producer blocks a page
   int prod_block = 0;                                 // producer block counter over the split
   // the first block (page 0) takes its page from pid0: the LDS page list is
   // read only after the prologue's barrier
@@ -267,7 +279,7 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
     r.rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(base), 0,
                                                pid >= 0 ? page_bytes : 0, kRsrcWord3);
     r.nval = page < np ? min(64, (t1 - t0) - page * 64) : 0;
-    r.idx0 = blk * RING;                              // first item of the block
+    r.idx0 = blk < nkb ? blk * KR : NK + (blk - nkb) * VR;   // first item of the block
     r.kind = page >= np ? 2 : (r.idx0 < NK ? 0 : 1);
     // key chunk c holds the 64 slots contiguously (2048 elements); M-tile m
     // of it is the 512-element run starting at m * 512.  Value tile u (16
@@ -297,9 +309,9 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
 
   u32x4 ring[RING];
   {
-    const ProdBlock pb0 = setup(prod_block++, true);
+    const ProdBlock pb0 = setup(prod_block++, true);     // page 0's first key block
 #pragma unroll
-    for (int s = 0; s < RING; ++s) ring[s] = issue(pb0, s);
+    for (int s = 0; s < KR; ++s) ring[s] = issue(pb0, s);
   }
 
   // ---- block-diagonal folded query (hi/lo bf16 MFMA B operands): the
@@ -349,22 +361,48 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
     floatx4 S[MPW];
 #pragma unroll
     for (int m = 0; m < MPW; ++m) S[m] = floatx4{0.f, 0.f, 0.f, 0.f};
-    for (int kb = 0; kb < NK; kb += RING) {
-      const ProdBlock pbk = setup(prod_block++);
-      u32x4 bhi = {0u, 0u, 0u, 0u}, blo = {0u, 0u, 0u, 0u};
+    // consume key slot s of the block at item kb
+    u32x4 bhi = {0u, 0u, 0u, 0u}, blo = {0u, 0u, 0u, 0u};
+    auto key_step = [&](int kb, int s) {
+      const int c = (kb + s) / MPW;       // position in the tile's chunk list
+      if (s % MPW == 0) {
+        const int pr = min(pair0_w + c, pmax_pair);
+        bhi = qblk[(pr * 2 + 0) * 64 + lane];
+        blo = qblk[(pr * 2 + 1) * 64 + lane];
+      }
+      u32x4 a = ring[s];
+      if (c == ci_last) a = keep_first(a, kvalid_last);
+      S[s % MPW] = mfma(a, bhi, S[s % MPW]);
+      S[s % MPW] = mfma(a, blo, S[s % MPW]);
+    };
+    if constexpr (KR == VR) {             // one block size: no block changes length
+      for (int kb = 0; kb < NK; kb += KR) {
+        const ProdBlock pbk = setup(prod_block++);
 #pragma unroll
-      for (int s = 0; s < RING; ++s) {
-        const int c = (kb + s) / MPW;     // chunk offset inside the tile's range
-        if (s % MPW == 0) {
-          const int pr = min(pair0_w + c, pmax_pair);
-          bhi = qblk[(pr * 2 + 0) * 64 + lane];
-          blo = qblk[(pr * 2 + 1) * 64 + lane];
+        for (int s = 0; s < KR; ++s) {
+          key_step(kb, s);
+          ring[s] = issue(pbk, s);
         }
-        u32x4 a = ring[s];
-        if (c == ci_last) a = keep_first(a, kvalid_last);
-        S[s % MPW] = mfma(a, bhi, S[s % MPW]);
-        S[s % MPW] = mfma(a, blo, S[s % MPW]);
-        ring[s] = issue(pbk, s);
+      }
+    } else {
+      int kb = 0;
+      for (; kb < NK - KR; kb += KR) {    // key block -> key block
+        const ProdBlock pbk = setup(prod_block++);
+#pragma unroll
+        for (int s = 0; s < KR; ++s) {
+          key_step(kb, s);
+          ring[s] = issue(pbk, s);
+        }
+      }
+      {                                   // last key block -> first value block
+        const ProdBlock pbv = setup(prod_block++);
+#pragma unroll
+        for (int s = KR; s < VR; ++s) ring[s] = issue(pbv, s);
+#pragma unroll
+        for (int s = 0; s < KR; ++s) {
+          key_step(kb, s);
+          if (s < VR) ring[s] = issue(pbv, s);
+        }
       }
     }
 
@@ -452,10 +490,15 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
 
     // ---- values: acc^T[rank][head] += Z_v^T[rank][tok] p^T[tok][head]
 #pragma unroll
-    for (int vb = 0; vb < NV; vb += RING) {
-      const ProdBlock pbv = setup(prod_block++);
+    for (int vb = 0; vb < NV; vb += VR) {
+      const ProdBlock pbn = setup(prod_block++);   // next block: values, or the next page's keys
+      const bool to_keys = vb + VR == NV;
+      if (to_keys) {
 #pragma unroll
-      for (int s = 0; s < RING; ++s) {
+        for (int s = VR; s < KR; ++s) ring[s] = issue(pbn, s);
+      }
+#pragma unroll
+      for (int s = 0; s < VR; ++s) {
         const int i = vb + s;
         const int mtl = i >> 1, ks = i & 1;
         u32x4 a = ring[s];
@@ -464,7 +507,7 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
 #pragma unroll
           for (int n = 0; n < NT; ++n) acc[mtl][n] = mfma(a, pB[n][ks], acc[mtl][n]);
         }
-        ring[s] = issue(pbv, s);
+        if (!to_keys || s < KR) ring[s] = issue(pbn, s);
       }
     }
   }
@@ -738,12 +781,12 @@ __global__ __launch_bounds__(256) void upproj(const float* __restrict__ amerged,
   }
 }
 
-template <int W, int NT, int MTW, int RING>
+template <int W, int NT, int MTW, int KR>
 hipError_t launch_split(const dckv_plan& p, const DecodeShape& sh, const u32x4* qblk,
                         const void* pool, int64_t num_pages, const int32_t* page_table,
                         int32_t max_pages, const int32_t* seq_lens, float* part_ml, float* part,
                         size_t lds, hipStream_t stream) {
-  auto kern = split_mfma<W, NT, MTW, RING>;
+  auto kern = split_mfma<W, NT, MTW, KR>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
   if (e != hipSuccess) return e;
@@ -767,9 +810,15 @@ hipError_t launch_split_r(const dckv_plan& p, const DecodeShape& sh, const u32x4
                           const void* pool, int64_t num_pages, const int32_t* page_table,
                           int32_t max_pages, const int32_t* seq_lens, float* part_ml, float* part,
                           size_t lds, hipStream_t stream) {
-  if (p.mfma.ring == 12)
-    return launch_split<W, NT, MTW, 12>(p, sh, qt, pool, num_pages, page_table, max_pages,
-                                        seq_lens, part_ml, part, lds, stream);
+  if constexpr (MTW <= 12) {               // the plan mixes block sizes only here
+    if (p.mfma.ring == 12)
+      return launch_split<W, NT, MTW, 12>(p, sh, qt, pool, num_pages, page_table, max_pages,
+                                          seq_lens, part_ml, part, lds, stream);
+    if (p.mfma.ring == 14)
+      return launch_split<W, NT, MTW, 14>(p, sh, qt, pool, num_pages, page_table, max_pages,
+                                          seq_lens, part_ml, part, lds, stream);
+  }
+  if (p.mfma.ring != 16) return hipErrorInvalidValue;
   return launch_split<W, NT, MTW, 16>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens,
                                       part_ml, part, lds, stream);
 }

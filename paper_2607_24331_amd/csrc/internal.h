@@ -47,7 +47,7 @@ struct MfmaTables {
   int32_t waves;                           // waves a work-group: 4 or 8
   int32_t mtw;                             // value M-tiles per wave: ceil(mt_v / waves)
   int32_t mtw_t;                           // compiled tile capacity: 6, 8, 12, 16 or 32 >= mtw
-  int32_t ring;                            // loads in flight a wave (12 or 16)
+  int32_t ring;                            // key block: loads in flight a wave (12, 14 or 16)
   int32_t max_pairs;                       // most LDS query blocks of any slice
   int32_t slice_heads[kMaxSlices];         // real rows in slice s
   int32_t hord[kMaxSlices][kSliceHeads];   // slot -> row i * H_q + h (query i, head h), -1 padding

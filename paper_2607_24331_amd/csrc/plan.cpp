@@ -89,18 +89,19 @@ bool place_rows(const dckv_plan& p, const std::vector<std::vector<int32_t>>& row
   return true;
 }
 
-// Items the slowest wave loads a page (key items padded to whole rings,
-// then the value items, also padded): the pace between the two softmax
-// barriers of a page.
+// Items the slowest wave loads a page: key items padded to whole key blocks
+// of `ring` loads (at least one block), then the value items padded to whole
+// value blocks (12 or 16 loads, fixed by the value-tile capacity).
 int32_t padded_items(const MfmaTables& t, int32_t ring) {
   const int32_t sw = std::min(4 * t.nt, t.waves), mpw = 4 * t.nt / sw;
-  int32_t nk_max = 0;
+  const int32_t vr = (2 * t.mtw_t) % 16 == 0 ? 16 : 12;
+  int32_t nk_max = ring == vr ? 0 : ring;
   for (int32_t s = 0; s < t.n_slices; ++s)
     for (int32_t n = 0; n < t.nt; ++n) {
       const int32_t nk = (t.kln[s][n][0] + t.kln[s][n][1]) * mpw;
       nk_max = std::max(nk_max, (nk + ring - 1) / ring * ring);
     }
-  return nk_max + (2 * t.mtw_t + ring - 1) / ring * ring;
+  return nk_max + (2 * t.mtw_t + vr - 1) / vr * vr;
 }
 
 }  // namespace
@@ -140,10 +141,10 @@ void build_mfma_tables(dckv_plan& p) {
   for (int32_t h = 0; h < p.Hq; ++h)
     for (int32_t i = 0; i < p.Q; ++i) rows_of[p.group_of_kv[h / p.qpk]].push_back(i * p.Hq + h);
 
-  // Group order and ring depth: the slowest wave's padded items a page
+  // Group order and key block size: the slowest wave's padded items a page
   // first, then the key chunks loaded by all tiles (a group cut by a tile
   // boundary is loaded by both tiles); ties keep the earlier candidate, so
-  // the group-id order and the deeper ring win.  Every order is tried for
+  // the group-id order and the longer block win.  Every order is tried for
   // up to seven groups; beyond that the group-id order alone.
   std::vector<int32_t> gorder(p.G);
   for (int32_t g = 0; g < p.G; ++g) gorder[g] = g;
@@ -153,7 +154,10 @@ void build_mfma_tables(dckv_plan& p) {
   do {
     int32_t total = 0;
     if (!place_rows(p, rows_of, gorder, J, per, cand, &total)) continue;
-    for (int32_t ring : {16, 12}) {
+    for (int32_t ring : {16, 14, 12}) {
+      // a key block longer or shorter than the value block costs registers:
+      // only value-tile capacities up to 12 leave room for it
+      if (t.mtw_t >= 16 && ring != 16) continue;
       const int32_t cost = padded_items(cand, ring);
       if (best_cost < 0 || cost < best_cost || (cost == best_cost && total < best_total)) {
         best = cand;
