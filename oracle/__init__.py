@@ -17,6 +17,8 @@ Modules
               (Sec. III-A, III-C, III-D), then textbook two-pass softmax
               attention in fp64
   dense       uncompressed paged K/V decode (the comparison baseline)
+  rope        decode with rotary position embedding on the rebuilt keys (a
+              reading: the paper never mentions positional encodings)
   compress    offline key compression, Algorithm 1: CKA head similarity,
               agglomerative clustering, energy ranks, greedy budget
               adjustment, per-group SVD, the cluster-count objective
@@ -26,8 +28,9 @@ Modules
 
 Parity status: every function here is pinned by the `-m "not gpu"` tests
 (closed forms, full-rank equivalence with uncompressed attention computed by
-a library routine, printed Table 1 figures, exhaustive/brute-force checks).
+a library routine, printed Table 1 figures, exhaustive/brute-force checks;
+the rotary reading by RoFormer's complex form and hand-worked rotations).
 """
 
 from . import bf16, bookkeeping, params, layout, append, attention, dense  # noqa: F401
-from . import compress, calibrate  # noqa: F401
+from . import compress, calibrate, rope  # noqa: F401
