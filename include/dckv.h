@@ -17,8 +17,9 @@
  *           multiplied once by the head's slice of R_v.
  *
  * Conventions of this library (readings where the paper is silent):
- *   - softmax scale 1/sqrt(d_h); no positional transform; no mask (a decode
- *     query attends to every cached token of its sequence);
+ *   - softmax scale 1/sqrt(d_h); no positional transform (dckv_decode_rope
+ *     below is the rotary variant); no mask (a decode query attends to
+ *     every cached token of its sequence);
  *   - query head h reads KV head floor(h / (H_q / H_kv));
  *   - the heads of group g are ordered by ascending KV-head index: the j-th
  *     of them owns columns [j*d_h, (j+1)*d_h) of R_g;
@@ -217,13 +218,50 @@ int dckv_decode(const dckv_plan* plan, const float* q, int32_t batch, const void
 
 /* Benchmark instrumentation (not part of the method).  With two non-NULL
  * hipEvent_t handles, every later dckv_decode on this plan launches its
- * split-K attention kernel (the dominant kernel of a decode) with `before`
+ * split-K attention kernel (the dominant kernel of a decode; for
+ * dckv_decode_rope the key-rebuild kernel) with `before`
  * and `after` as the dispatch's own start and stop events
  * (hipExtLaunchKernel), so their interval is that kernel's execution alone;
  * NULL handles switch this off.  The
  * events stay owned by the caller.  A plan being instrumented must not be
  * used by several threads at once.  Makes no HIP call itself. */
 int dckv_plan_set_profile_events(dckv_plan* plan, void* before, void* after);
+
+/* ------------------------------------------------------------------------
+ * Decode with rotary position embedding on the keys.  The paper never
+ * mentions positional encodings; this is the reading for models that rotate
+ * keys per position.  The factorisation of Sec. III-C is taken to be of the
+ * key projection before the rotation, so the cache layout, the append and
+ * the factors are those above.  The key of cache position t for query
+ * head h is K_h[t] = Rot(t)(z_t R_{g,h}), and the query q_h is rotated to the
+ * newest position, Rot(T_b - 1) q_h.  Rot(pos) turns each plane of
+ * coordinates (i, i + d_h/2), i < d_h/2, by the angle
+ * pos * rope_base^(-2i/d_h) (RoFormer's rotary embedding, rotate-half
+ * pairing):
+ *   x'_i = x_i cos - x_{i+d_h/2} sin,   x'_{i+d_h/2} = x_{i+d_h/2} cos + x_i sin.
+ * Values are not rotated.  Softmax scale, head map and the rest are as for
+ * dckv_decode.  A rotation that depends on t cannot be folded into the query
+ * once, so each key is rebuilt per token (r_g * d_h MACs a token and KV head,
+ * on MFMA), turned and dotted with the turned query.  Angles are reduced in
+ * fp64 before the fp32 sine and cosine.
+ *
+ * Requirements: a bf16 plan on the MFMA path (geometry mfma_path == 1),
+ * queries_per_seq 1, d_h 64 or 128, at most 8 query heads a KV head,
+ * rope_base a finite number above 1.  Context splits are those of
+ * dckv_decode capped at 1024 tokens.  Arguments, ownership, validation
+ * (DCKV_EINVAL, DCKV_EALIGN, DCKV_EWORKSPACE, DCKV_EHIP; nothing enqueued on
+ * error) and reproducibility as for dckv_decode (q and out [batch, H_q, d_h]
+ * fp32), with a workspace of dckv_rope_workspace_bytes.  The workspace
+ * also receives the factors R_g transposed into MFMA operand blocks, rebuilt
+ * on every call.  With profile events set on the plan, the key-rebuild
+ * kernel is the one stamped. */
+int dckv_rope_workspace_bytes(const dckv_plan* plan, int32_t batch, int32_t max_context,
+                              size_t* bytes);
+int dckv_decode_rope(const dckv_plan* plan, const float* q, int32_t batch, const void* pool,
+                     int64_t num_pages, const int32_t* page_table, int32_t max_pages,
+                     const int32_t* seq_lens, int32_t max_context, const void* R_keys,
+                     const void* R_value, double rope_base, float* out, void* workspace,
+                     size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * Uncompressed baseline (no compression): decode over a paged bf16 K/V

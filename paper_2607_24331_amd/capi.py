@@ -84,6 +84,9 @@ SIGNATURES = {
     "dckv_decode": (ctypes.c_int, [_vp, _vp, _i32, _vp, _i64, _vp, _i32, _vp, _i32, _vp, _vp, _vp,
                                    _vp, ctypes.c_size_t, _vp]),
     "dckv_plan_set_profile_events": (ctypes.c_int, [_vp, _vp, _vp]),
+    "dckv_rope_workspace_bytes": (ctypes.c_int, [_vp, _i32, _i32, ctypes.POINTER(ctypes.c_size_t)]),
+    "dckv_decode_rope": (ctypes.c_int, [_vp, _vp, _i32, _vp, _i64, _vp, _i32, _vp, _i32, _vp, _vp,
+                                        ctypes.c_double, _vp, _vp, ctypes.c_size_t, _vp]),
     "dckv_dense_page_elems": (ctypes.c_int, [_i32, _i32, ctypes.POINTER(ctypes.c_int64)]),
     "dckv_dense_workspace_bytes": (ctypes.c_int, [_i32, _i32, _i32, _i32, _i32, _i32,
                                                   ctypes.POINTER(ctypes.c_size_t)]),

@@ -156,13 +156,18 @@ __global__ __launch_bounds__(64) void fold_blocks(const float* __restrict__ q,
 // (16 ranks) a wave; key ring blocks of KR loads, value ring blocks of VR
 // (12 or 16, whichever holds the 2 MTW value items of a page without
 // padding, or with the least).
-template <int W, int NT, int MTW, int KR>
+// PW (the rotary decode's value pass): the split's softmax weights come
+// ready from pw ([slot][split_tokens] bf16 per (sequence, slice, split),
+// relative to the split maximum, with m and l already in part_ml), so there
+// is no key phase and no online softmax: the whole split's weights are
+// staged in LDS once, and the pages stream values only (KR == VR).
+template <int W, int NT, int MTW, int KR, bool PW = false>
 __global__ __launch_bounds__(W * 64, 1) void split_mfma(
     const u32x4* __restrict__ qblk_ws, const bf16* __restrict__ pool, int64_t num_pages,
     const int32_t* __restrict__ page_table, int max_pages, const int32_t* __restrict__ seq_lens,
     int max_context, int split_tokens, int n_split, int n_units, int RK, int rv,
     int64_t page_elems, int64_t value_base, float* __restrict__ part_ml, float* __restrict__ part,
-    MfmaTables mt) {
+    MfmaTables mt, const bf16* __restrict__ pw) {
   constexpr int NH = 16 * NT;                          // head slots of the slice
   constexpr int SW = (4 * NT < W) ? 4 * NT : W;        // waves holding score tiles
   constexpr int MPW = (4 * NT) / SW;                   // score M-tiles (16 tokens) a scoring wave
@@ -170,6 +175,7 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
   constexpr int RING = KR > VR ? KR : VR;              // ring slots
   constexpr int NV = ((2 * MTW + VR - 1) / VR) * VR;   // value items a page (padded)
   static_assert(KR % 2 == 0 && KR % MPW == 0 && VR % 2 == 0, "blocks hold whole chunks and k-steps");
+  static_assert(!PW || KR == VR, "the weighted value pass streams values only");
   extern __shared__ __align__(16) unsigned char smem[];
 
   const int J = mt.n_slices;
@@ -186,12 +192,15 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
 
   // ---- LDS carve-up
   const int nch0 = mt.kln[slice][0][0] + mt.kln[slice][0][1];
-  const int npairs = nch0 + (NT > 1 ? mt.kln[slice][1][0] + mt.kln[slice][1][1] : 0);
+  const int npairs = PW ? 0 : nch0 + (NT > 1 ? mt.kln[slice][1][0] + mt.kln[slice][1][1] : 0);
   u32x4* qblk = reinterpret_cast<u32x4*>(smem);                         // [npairs][2][64]
   bf16* p_lds = reinterpret_cast<bf16*>(smem + size_t(npairs) * 2048);  // [32][kPStride]
   float* red_max = reinterpret_cast<float*>(p_lds + 32 * kPStride);     // [8][32]
   float* red_sum = red_max + 8 * 32;                                    // [8][32]
   int* pids = reinterpret_cast<int*>(red_sum + 8 * 32);                 // [kPageSlots]
+  // PW: the split's weights [NH][split_tokens + 8] (16-byte row pad) after the page list
+  const int pst = split_tokens + 8;
+  bf16* p_all = reinterpret_cast<bf16*>(pids + kPageSlots);
 
   // ---- the prologue's loads go out together, none waiting on another:
   // this lane's query row (for the causal limit) and page-table entry, the
@@ -208,8 +217,10 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
   const u32x4* qsrc = qblk_ws + int64_t(b * J + slice) * mt.max_pairs * 128;
   const int n16 = npairs * 128;
   u32x4 qv[kQblkLoads];
+  if constexpr (!PW) {
 #pragma unroll
-  for (int k = 0; k < kQblkLoads; ++k) qv[k] = qsrc[min(tid + k * W * 64, n16 - 1)];
+    for (int k = 0; k < kQblkLoads; ++k) qv[k] = qsrc[min(tid + k * W * 64, n16 - 1)];
+  }
   int pid0 = (t0 >> 6) < max_pages ? page_table[int64_t(b) * max_pages + (t0 >> 6)] : -1;
   pid0 = __builtin_amdgcn_readfirstlane((pid0 >= 0 && pid0 < num_pages) ? pid0 : -1);
   int T_b = seq_lens[b];
@@ -230,7 +241,7 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
   const int st0_w = mt.kst[slice][n_w][0], ln0_w = mt.kln[slice][n_w][0];
   const int st1_w = mt.kst[slice][n_w][1];
   const int nch_w = ln0_w + mt.kln[slice][n_w][1];
-  const int nk_real = scoring ? nch_w * MPW : 0;      // key items a page
+  const int nk_real = (scoring && !PW) ? nch_w * MPW : 0;   // key items a page
   // key items padded to whole blocks; with two block sizes every wave has at
   // least one key block (all-dummy for a wave without score tiles), so the
   // last key block's change of length is on every wave's schedule
@@ -314,17 +325,39 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
     for (int s = 0; s < KR; ++s) ring[s] = issue(pb0, s);
   }
 
+  if constexpr (PW) {
+    // ---- the split's weights into LDS, eight loads in flight a thread;
+    // padding slots (no query head) get zero weights
+    const bf16* src = pw + (int64_t(b * J + slice) * n_split + split) * NH * split_tokens;
+    const int vrow = split_tokens / 8, nvec = NH * vrow;
+    for (int base = tid; base < nvec; base += 8 * W * 64) {
+      u32x4 v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) v[k] = *reinterpret_cast<const u32x4*>(src + 8 * min(base + k * W * 64, nvec - 1));
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int idx = base + k * W * 64;
+        if (idx < nvec) {
+          const int slot = idx / vrow, col = idx - slot * vrow;
+          *reinterpret_cast<u32x4*>(p_all + slot * pst + 8 * col) =
+              mt.hord[slice][slot] >= 0 ? v[k] : u32x4{0u, 0u, 0u, 0u};
+        }
+      }
+    }
+  }
   // ---- block-diagonal folded query (hi/lo bf16 MFMA B operands): the
   // registers loaded above go to LDS (their loads precede the ring's, so
   // the ring stays in flight); a plan with more blocks than the registers
   // hold copies the rest here, eight loads in flight a thread.
+  if constexpr (!PW) {
 #pragma unroll
   for (int k = 0; k < kQblkLoads; ++k) {
     const int idx = tid + k * W * 64;
     if (idx < n16) qblk[idx] = qv[k];
   }
+  }
   {
-    for (int base = tid + kQblkLoads * W * 64; base < n16; base += 8 * W * 64) {
+    for (int base = tid + kQblkLoads * W * 64; base < n16 && !PW; base += 8 * W * 64) {
       u32x4 v[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
@@ -356,6 +389,14 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
   for (int page = 0; page < np; ++page) {
     const int nval = min(64, (t1 - t0) - page * 64);
     const bool pvalid = pids[page] >= 0;
+    u32x4 pB[NT][2];
+    if constexpr (PW) {                   // weights ready in LDS: no keys, no softmax
+#pragma unroll
+      for (int n = 0; n < NT; ++n)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+          pB[n][ks] = *reinterpret_cast<const u32x4*>(p_all + (16 * n + lr) * pst + 64 * page + 32 * ks + 8 * lq);
+    } else {
 
     // ---- scores: MPW M-tiles (16 tokens each) of this wave's N-tile
     floatx4 S[MPW];
@@ -472,7 +513,6 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
       m_run[n] = m_new[n];
       rescale = rescale || alpha[n] != 1.f;
     }
-    u32x4 pB[NT][2];
 #pragma unroll
     for (int n = 0; n < NT; ++n)
 #pragma unroll
@@ -484,6 +524,7 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
 #pragma unroll
         for (int n = 0; n < NT; ++n) acc[i][n] *= alpha[n];
     }
+    }                                     // !PW
     // token masks of the two k-steps on a partial page
     const int keep0 = min(8, max(0, nval - 8 * lq));
     const int keep1 = min(8, max(0, nval - 32 - 8 * lq));
@@ -518,8 +559,11 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
     float* pml = part_ml + prow * (2 * NH);
 #pragma unroll
     for (int n = 0; n < NT; ++n) {
-      pml[16 * n + lane] = m_run[n];
-      pml[NH + 16 * n + lane] = l_run[n];
+      // PW: the key-rebuild kernel wrote the slots of real heads
+      if (!PW || mt.hord[slice][16 * n + lane] < 0) {
+        pml[16 * n + lane] = m_run[n];
+        pml[NH + 16 * n + lane] = l_run[n];
+      }
     }
   }
   float* pa = part + prow * int64_t(NH) * rv;
@@ -785,7 +829,21 @@ template <int W, int NT, int MTW, int KR>
 hipError_t launch_split(const dckv_plan& p, const DecodeShape& sh, const u32x4* qblk,
                         const void* pool, int64_t num_pages, const int32_t* page_table,
                         int32_t max_pages, const int32_t* seq_lens, float* part_ml, float* part,
-                        size_t lds, hipStream_t stream) {
+                        size_t lds, hipStream_t stream, const bf16* pw = nullptr) {
+  if (pw) {                               // the rotary decode's value pass
+    if constexpr (KR == (((2 * MTW) % 16 == 0) ? 16 : 12)) {
+      auto kern = split_mfma<W, NT, MTW, KR, true>;
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(kern, dim3(sh.n_units * p.mfma.n_slices), dim3(W * 64), lds, stream, qblk,
+                         static_cast<const bf16*>(pool), num_pages, page_table, max_pages, seq_lens,
+                         sh.max_context, sh.split_tokens, sh.n_split, sh.batch * sh.n_split, p.RK,
+                         p.rv, p.page_elems, p.value_base, part_ml, part, p.mfma, pw);
+      return hipGetLastError();
+    }
+    return hipErrorInvalidValue;
+  }
   auto kern = split_mfma<W, NT, MTW, KR>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
@@ -796,12 +854,13 @@ hipError_t launch_split(const dckv_plan& p, const DecodeShape& sh, const u32x4* 
                           p.prof_after, 0u, qblk, static_cast<const bf16*>(pool), num_pages,
                           page_table, max_pages, seq_lens, sh.max_context, sh.split_tokens,
                           sh.n_split, sh.batch * sh.n_split, p.RK, p.rv, p.page_elems,
-                          p.value_base, part_ml, part, p.mfma);
+                          p.value_base, part_ml, part, p.mfma, static_cast<const bf16*>(nullptr));
   else
     hipLaunchKernelGGL(kern, dim3(grid), dim3(W * 64), lds, stream, qblk,
                        static_cast<const bf16*>(pool), num_pages, page_table, max_pages, seq_lens,
                        sh.max_context, sh.split_tokens, sh.n_split, sh.batch * sh.n_split, p.RK,
-                       p.rv, p.page_elems, p.value_base, part_ml, part, p.mfma);
+                       p.rv, p.page_elems, p.value_base, part_ml, part, p.mfma,
+                       static_cast<const bf16*>(nullptr));
   return hipGetLastError();
 }
 
@@ -842,6 +901,54 @@ hipError_t launch_split_w(const dckv_plan& p, const DecodeShape& sh, const u32x4
   return hipErrorInvalidValue;
 }
 
+// The rotary decode's value pass: the split kernel with weights from the
+// workspace, its value ring block fixed by the value tiles a wave.
+template <int W, int NT>
+hipError_t launch_split_pw(const dckv_plan& p, const DecodeShape& sh, const void* pool,
+                           int64_t num_pages, const int32_t* page_table, int32_t max_pages,
+                           const int32_t* seq_lens, float* part_ml, float* part, const bf16* pw,
+                           size_t lds, hipStream_t stream) {
+#define DCKV_PW(M)                                                                             \
+  return launch_split<W, NT, M, ((2 * (M)) % 16 == 0 ? 16 : 12)>(                              \
+      p, sh, nullptr, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, lds, \
+      stream, pw)
+  switch (p.mfma.mtw_t) {
+    case 6: DCKV_PW(6);
+    case 8: DCKV_PW(8);
+    case 12: DCKV_PW(12);
+    case 16: DCKV_PW(16);
+    case 32: DCKV_PW(NT == 1 ? 32 : 16);
+  }
+#undef DCKV_PW
+  return hipErrorInvalidValue;
+}
+
+// Merge of the splits' partials and the up-projection by R_v, shared by the
+// position-free and the rotary decode.
+hipError_t launch_merge_upproj(const dckv_plan& p, const DecodeShape& sh, const int32_t* seq_lens,
+                               const float* part_ml, const float* part, float* amerged,
+                               const void* R_value, float* out, hipStream_t stream) {
+  if (p.mfma.nt == 1)
+    hipLaunchKernelGGL(merge_mfma<16>, dim3(sh.batch * p.mfma.n_slices, sh.n_rchunks), dim3(256), 0,
+                       stream, part_ml, part, seq_lens, sh.max_context, sh.split_tokens,
+                       sh.n_split, p.rv, amerged, p.tables, p.mfma);
+  else
+    hipLaunchKernelGGL(merge_mfma<32>, dim3(sh.batch * p.mfma.n_slices, sh.n_rchunks), dim3(256), 0,
+                       stream, part_ml, part, seq_lens, sh.max_context, sh.split_tokens,
+                       sh.n_split, p.rv, amerged, p.tables, p.mfma);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int rows = sh.batch * p.Q * p.qpk;            // (sequence, query, head of a KV head)
+  const size_t lds_up = (size_t(8) * p.rv + 64 * 8 * 32) * sizeof(float);
+  e = hipFuncSetAttribute(reinterpret_cast<const void*>(upproj),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, int(lds_up));
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(upproj, dim3((rows + 7) / 8, p.Hkv, (p.dh + 31) / 32), dim3(256), lds_up,
+                     stream, amerged, static_cast<const bf16*>(R_value), out, sh.batch * p.Q,
+                     p.rv, p.tables);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 size_t mfma_split_lds_bytes(const dckv_plan& p) {
@@ -876,24 +983,42 @@ hipError_t launch_decode_mfma(const dckv_plan& p, const DecodeShape& sh, const f
             ? launch_split_w<8, 1>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, lds, stream)
             : launch_split_w<8, 2>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, lds, stream);
   if (e != hipSuccess) return e;
-  if (p.mfma.nt == 1)
-    hipLaunchKernelGGL(merge_mfma<16>, dim3(sh.batch * p.mfma.n_slices, sh.n_rchunks), dim3(256), 0,
-                       stream, part_ml, part, seq_lens, sh.max_context, sh.split_tokens,
-                       sh.n_split, p.rv, amerged, p.tables, p.mfma);
-  else
-    hipLaunchKernelGGL(merge_mfma<32>, dim3(sh.batch * p.mfma.n_slices, sh.n_rchunks), dim3(256), 0,
-                       stream, part_ml, part, seq_lens, sh.max_context, sh.split_tokens,
-                       sh.n_split, p.rv, amerged, p.tables, p.mfma);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  const int rows = sh.batch * p.Q * p.qpk;            // (sequence, query, head of a KV head)
-  const size_t lds_up = (size_t(8) * p.rv + 64 * 8 * 32) * sizeof(float);
-  e = hipFuncSetAttribute(reinterpret_cast<const void*>(upproj),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, int(lds_up));
+  return launch_merge_upproj(p, sh, seq_lens, part_ml, part, amerged, R_value, out, stream);
+}
+
+size_t rope_value_lds_bytes(const dckv_plan& p, int32_t split_tokens) {
+  // the split kernel's fixed carve-up without query blocks, then the weights
+  return size_t(32) * kPStride * 2 + 2 * 8 * 32 * 4 + kPageSlots * 4 +
+         size_t(16) * p.mfma.nt * (split_tokens + 8) * 2;
+}
+
+hipError_t launch_decode_rope(const dckv_plan& p, const DecodeShape& sh, const float* q,
+                              const void* pool, int64_t num_pages, const int32_t* page_table,
+                              int32_t max_pages, const int32_t* seq_lens, const void* R_keys,
+                              const void* R_value, double rope_base, float* out, void* workspace,
+                              hipStream_t stream) {
+  char* ws = static_cast<char*>(workspace);
+  void* rt = ws + sh.off_rt;
+  bf16* pw = reinterpret_cast<bf16*>(ws + sh.off_p);
+  float* part_ml = reinterpret_cast<float*>(ws + sh.off_ml);
+  float* part = reinterpret_cast<float*>(ws + sh.off_acc);
+  float* amerged = reinterpret_cast<float*>(ws + sh.off_opart);
+  hipError_t e = launch_rope_factors(p, R_keys, rt, stream);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(upproj, dim3((rows + 7) / 8, p.Hkv, (p.dh + 31) / 32), dim3(256), lds_up,
-                     stream, amerged, static_cast<const bf16*>(R_value), out, sh.batch * p.Q,
-                     p.rv, p.tables);
-  return hipGetLastError();
+  e = launch_rope_scores(p, sh, q, pool, num_pages, page_table, max_pages, seq_lens, rt, rope_base,
+                         pw, part_ml, stream);
+  if (e != hipSuccess) return e;
+  const size_t lds = rope_value_lds_bytes(p, sh.split_tokens);
+  if (p.mfma.waves == 4)
+    e = p.mfma.nt == 1
+            ? launch_split_pw<4, 1>(p, sh, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, pw, lds, stream)
+            : launch_split_pw<4, 2>(p, sh, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, pw, lds, stream);
+  else
+    e = p.mfma.nt == 1
+            ? launch_split_pw<8, 1>(p, sh, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, pw, lds, stream)
+            : launch_split_pw<8, 2>(p, sh, pool, num_pages, page_table, max_pages, seq_lens, part_ml, part, pw, lds, stream);
+  if (e != hipSuccess) return e;
+  return launch_merge_upproj(p, sh, seq_lens, part_ml, part, amerged, R_value, out, stream);
 }
 
 }  // namespace dckv

@@ -55,6 +55,26 @@ struct MfmaTables {
   int32_t kln[kMaxSlices][2][2];           // chunks in each range (0 for an unused range)
 };
 
+// Per-head facts of the rotary decode (rope.hip), built with the plan.  The
+// key-rebuild kernel reads, for each KV head, the transposed factor blocks
+// of its group: for every 32-column key chunk that meets the group's
+// columns and every 16-row tile of the head's d_h rows, one 16 x 32 bf16
+// block in MFMA A-operand order (zero outside the group's columns).
+struct RopeTables {
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t q_per_kv;
+  int32_t nh;                               // head slots a slice (16 * nt)
+  int32_t koff[DCKV_MAX_HEADS];             // per KV head: first key column of its group
+  int32_t rank[DCKV_MAX_HEADS];             // r_g of its group
+  int32_t rcol[DCKV_MAX_HEADS];             // first column of the head inside R_g
+  int32_t rstride[DCKV_MAX_HEADS];          // row length of R_g: h_g * d_h
+  int32_t rt_off[DCKV_MAX_HEADS];           // element offset of the head's transposed blocks
+  int32_t work_kv[DCKV_MAX_HEADS];          // KV heads in work order (group by group)
+  int32_t qslot[DCKV_MAX_HEADS];            // query head -> slice * 32 + slot
+  int64_t roff[DCKV_MAX_HEADS];             // per KV head: element offset of R_g
+};
+
 // Launch shape of one decode call, fixed by the plan and (batch, max_context).
 struct DecodeShape {
   int32_t batch;
@@ -68,6 +88,8 @@ struct DecodeShape {
   size_t off_ml;
   size_t off_acc;
   size_t off_opart;
+  size_t off_rt;            // rotary decode: transposed key factors
+  size_t off_p;             // rotary decode: softmax weights of each split (bf16)
   size_t bytes;
 };
 
@@ -92,6 +114,8 @@ struct dckv_plan {
   bool mfma_ok = false;              // bf16 MFMA decode path applies
   dckv::MfmaTables mfma{};
   int32_t key_chunk_loads = 0;       // key chunks the MFMA tiles load a page
+  dckv::RopeTables rope{};           // rotary decode tables (valid with mfma_ok)
+  int64_t rope_rt_elems = 0;         // elements of the transposed key factors
   hipEvent_t prof_before = nullptr;  // benchmark instrumentation of the split kernel
   hipEvent_t prof_after = nullptr;
 };
@@ -120,6 +144,22 @@ hipError_t launch_decode_mfma(const dckv_plan& p, const DecodeShape& sh, const f
                               const void* pool, int64_t num_pages, const int32_t* page_table,
                               int32_t max_pages, const int32_t* seq_lens, const void* R_keys,
                               const void* R_value, float* out, void* workspace, hipStream_t stream);
+
+// Rotary decode (rope.hip, decode_mfma.hip).
+void build_rope_tables(dckv_plan& p);
+DecodeShape rope_shape(const dckv_plan& p, int32_t batch, int32_t max_context);
+int rope_max_q_per_kv();
+size_t rope_value_lds_bytes(const dckv_plan& p, int32_t split_tokens);
+hipError_t launch_rope_factors(const dckv_plan& p, const void* R_keys, void* rt, hipStream_t stream);
+hipError_t launch_rope_scores(const dckv_plan& p, const DecodeShape& sh, const float* q,
+                              const void* pool, int64_t num_pages, const int32_t* page_table,
+                              int32_t max_pages, const int32_t* seq_lens, const void* rt,
+                              double rope_base, void* pbuf, float* part_ml, hipStream_t stream);
+hipError_t launch_decode_rope(const dckv_plan& p, const DecodeShape& sh, const float* q,
+                              const void* pool, int64_t num_pages, const int32_t* page_table,
+                              int32_t max_pages, const int32_t* seq_lens, const void* R_keys,
+                              const void* R_value, double rope_base, float* out, void* workspace,
+                              hipStream_t stream);
 
 // Defined in the kernel sources.
 DecodeShape decode_shape(const dckv_plan& p, int32_t batch, int32_t max_context);

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <new>
@@ -175,6 +176,44 @@ void build_mfma_tables(dckv_plan& p) {
   p.mfma_ok = true;
 }
 
+// Tables of the rotary decode: per KV head its group's key columns and
+// factor block, the offset of its transposed factor blocks (one 16 x 32
+// block per key chunk meeting the group's columns and per 16 rows of d_h),
+// the heads in group order, and each query head's slot in the MFMA slices.
+void build_rope_tables(dckv_plan& p) {
+  p.rope = RopeTables{};
+  p.rope_rt_elems = 0;
+  if (!p.mfma_ok) return;
+  RopeTables& r = p.rope;
+  r.n_kv_heads = p.Hkv;
+  r.head_dim = p.dh;
+  r.q_per_kv = p.qpk;
+  r.nh = 16 * p.mfma.nt;
+  int32_t n = 0;
+  for (int32_t g = 0; g < p.G; ++g)
+    for (int32_t kv = 0; kv < p.Hkv; ++kv)
+      if (p.group_of_kv[kv] == g) r.work_kv[n++] = kv;
+  int64_t off = 0;
+  for (int32_t kv = 0; kv < p.Hkv; ++kv) {
+    const int32_t g = p.group_of_kv[kv];
+    r.koff[kv] = p.koff[g];
+    r.rank[kv] = p.ranks[g];
+    r.rcol[kv] = p.pos_in_group[kv] * p.dh;
+    r.rstride[kv] = p.hg[g] * p.dh;
+    r.roff[kv] = p.roff[g];
+    r.rt_off[kv] = int32_t(off);
+    const int32_t nch = (p.koff[g] + p.ranks[g] - 1) / 32 - p.koff[g] / 32 + 1;
+    off += int64_t(nch) * p.dh * 32;
+  }
+  p.rope_rt_elems = off;
+  for (int32_t h = 0; h < DCKV_MAX_HEADS; ++h) r.qslot[h] = -1;
+  for (int32_t sl = 0; sl < p.mfma.n_slices; ++sl)
+    for (int32_t j2 = 0; j2 < kSliceHeads; ++j2) {
+      const int32_t row = p.mfma.hord[sl][j2];
+      if (row >= 0 && row < p.Hq) r.qslot[row] = sl * 32 + j2;   // query 0's rows
+    }
+}
+
 }  // namespace dckv
 
 extern "C" {
@@ -300,6 +339,7 @@ int dckv_plan_create(const dckv_layer_desc* d, dckv_plan** out) {
     return fail(DCKV_ENOMEM, "plan_create: host allocation failed");
   }
   dckv::build_mfma_tables(*p);
+  dckv::build_rope_tables(*p);
   *out = p;
   return DCKV_OK;
 }
@@ -401,6 +441,64 @@ int dckv_decode(const dckv_plan* p, const float* q, int32_t batch, const void* p
   hipError_t e = dckv::launch_decode(*p, shape, q, pool, num_pages, page_table, max_pages, seq_lens,
                                      R_keys, R_value, out, workspace, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(DCKV_EHIP, "decode: %s", hipGetErrorString(e));
+  return DCKV_OK;
+}
+
+// ------------------------------------------------ rotary decode
+static int rope_check(const char* where, const dckv_plan* p) {
+  if (!p) return fail(DCKV_EINVAL, "%s: null plan", where);
+  if (!p->mfma_ok)
+    return fail(DCKV_EINVAL, "%s: the rotary decode runs on the bf16 MFMA path, which this plan does not take", where);
+  if (p->Q != 1) return fail(DCKV_EINVAL, "%s: one query a sequence (the plan has %d)", where, p->Q);
+  if (p->dh != 64 && p->dh != 128) return fail(DCKV_EINVAL, "%s: head_dim %d is not 64 or 128", where, p->dh);
+  if (p->qpk > dckv::rope_max_q_per_kv())
+    return fail(DCKV_EINVAL, "%s: %d query heads a KV head (at most %d)", where, p->qpk, dckv::rope_max_q_per_kv());
+  for (int32_t h = 0; h < p->Hq; ++h)   // every head owns a slot of the MFMA slices
+    if (p->rope.qslot[h] < 0) return fail(DCKV_EINVAL, "%s: query head %d has no MFMA slot", where, h);
+  return DCKV_OK;
+}
+
+int dckv_rope_workspace_bytes(const dckv_plan* p, int32_t batch, int32_t max_context, size_t* bytes) {
+  int st = rope_check("rope_workspace_bytes", p);
+  if (st != DCKV_OK) return st;
+  if (!bytes) return fail(DCKV_EINVAL, "rope_workspace_bytes: null bytes pointer");
+  if (batch < 0 || max_context < 0)
+    return fail(DCKV_EINVAL, "rope_workspace_bytes: negative batch %d or max_context %d", batch, max_context);
+  *bytes = dckv::rope_shape(*p, batch, max_context).bytes;
+  return DCKV_OK;
+}
+
+int dckv_decode_rope(const dckv_plan* p, const float* q, int32_t batch, const void* pool,
+                     int64_t num_pages, const int32_t* page_table, int32_t max_pages,
+                     const int32_t* seq_lens, int32_t max_context, const void* R_keys,
+                     const void* R_value, double rope_base, float* out, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+  int st = rope_check("decode_rope", p);
+  if (st != DCKV_OK) return st;
+  if (!(rope_base > 1.0) || !std::isfinite(rope_base))
+    return fail(DCKV_EINVAL, "decode_rope: rope_base %g is not a finite number above 1", rope_base);
+  if (batch < 0) return fail(DCKV_EINVAL, "decode_rope: batch %d < 0", batch);
+  if (batch == 0) return DCKV_OK;
+  if (!q || !pool || !page_table || !seq_lens || !R_keys || !R_value || !out || !workspace)
+    return fail(DCKV_EINVAL, "decode_rope: null device pointer");
+  if (batch > 65535) return fail(DCKV_EINVAL, "decode_rope: batch %d above 65535", batch);
+  if (num_pages < 1) return fail(DCKV_EINVAL, "decode_rope: num_pages %lld < 1", (long long)num_pages);
+  if (max_pages < 1) return fail(DCKV_EINVAL, "decode_rope: max_pages %d < 1", max_pages);
+  if (max_context < 0 || int64_t(max_context) > int64_t(max_pages) * DCKV_PAGE_TOKENS)
+    return fail(DCKV_EINVAL, "decode_rope: max_context %d outside [0, max_pages*64 = %lld]", max_context,
+                (long long)max_pages * DCKV_PAGE_TOKENS);
+  if (!aligned(q, 16) || !aligned(pool, 16) || !aligned(R_keys, 16) || !aligned(R_value, 16) ||
+      !aligned(out, 16) || !aligned(page_table, 4) || !aligned(seq_lens, 4))
+    return fail(DCKV_EALIGN, "decode_rope: q, pool, R_keys, R_value and out must be 16-byte aligned");
+  if (!aligned(workspace, 256)) return fail(DCKV_EALIGN, "decode_rope: workspace must be 256-byte aligned");
+  const dckv::DecodeShape shape = dckv::rope_shape(*p, batch, max_context);
+  if (workspace_bytes < shape.bytes)
+    return fail(DCKV_EWORKSPACE, "decode_rope: workspace of %zu bytes, %zu needed", workspace_bytes,
+                shape.bytes);
+  hipError_t e = dckv::launch_decode_rope(*p, shape, q, pool, num_pages, page_table, max_pages,
+                                          seq_lens, R_keys, R_value, rope_base, out, workspace,
+                                          static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(DCKV_EHIP, "decode_rope: %s", hipGetErrorString(e));
   return DCKV_OK;
 }
 

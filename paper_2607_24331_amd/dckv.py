@@ -94,6 +94,12 @@ class Plan:
                "decode_workspace_bytes")
         return n.value
 
+    def rope_workspace_bytes(self, batch: int, max_context: int) -> int:
+        n = ctypes.c_size_t()
+        _check(_lib.dckv_rope_workspace_bytes(self.handle, batch, max_context, ctypes.byref(n)),
+               "rope_workspace_bytes")
+        return n.value
+
     def new_pool(self, num_pages: int, device="cuda") -> torch.Tensor:
         """Zero-filled pool of `num_pages` pages."""
         return torch.zeros((num_pages, self.page_elems), dtype=self.torch_dtype, device=device)
@@ -200,6 +206,41 @@ def decode(plan: Plan, q: torch.Tensor, pool: torch.Tensor, page_table: torch.Te
     _check(_lib.dckv_decode(plan.handle, pq, B, pp, _num_pages(plan, pool), pt, page_table.shape[1],
                             psl, int(max_context), prk, prv, po, pw, workspace.numel(),
                             _stream_handle(stream)), "decode")
+    return out
+
+
+def decode_rope(plan: Plan, q: torch.Tensor, pool: torch.Tensor, page_table: torch.Tensor,
+                seq_lens: torch.Tensor, max_context: int, R_keys: torch.Tensor,
+                R_value: torch.Tensor, rope_base: float = 10000.0,
+                out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                stream=None) -> torch.Tensor:
+    """Decode with rotary position embedding on the keys (q and the result
+    [batch, H_q, d_h] fp32): key t turned by Rot(t), the query by
+    Rot(seq_len - 1), planes (i, i + d_h/2) at angle pos * rope_base^(-2i/d_h)."""
+    B = q.shape[0]
+    qshape = (B, plan.num_q_heads, plan.head_dim)
+    dt = plan.torch_dtype
+    pq = _dev(q, "q", torch.float32, qshape)
+    pp = _dev(pool, "pool", dt)
+    if page_table.dim() != 2 or page_table.shape[0] != B:
+        raise ValueError("page_table must be [batch, max_pages]")
+    pt = _dev(page_table, "page_table", torch.int32)
+    psl = _dev(seq_lens, "seq_lens", torch.int32, (B,))
+    prk = _dev(R_keys, "R_keys", dt)
+    if R_keys.numel() != plan.key_factor_elems:
+        raise ValueError(f"R_keys holds {R_keys.numel()} elements, expected {plan.key_factor_elems}")
+    prv = _dev(R_value, "R_value", dt, (plan.value_rank, plan.num_kv_heads * plan.head_dim))
+    if out is None:
+        out = torch.empty(qshape, dtype=torch.float32, device=q.device)
+    po = _dev(out, "out", torch.float32, qshape)
+    need = plan.rope_workspace_bytes(B, max_context)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=q.device)
+    pw = _dev(workspace, "workspace", torch.uint8)
+    _check(_lib.dckv_decode_rope(plan.handle, pq, B, pp, _num_pages(plan, pool), pt,
+                                 page_table.shape[1], psl, int(max_context), prk, prv,
+                                 float(rope_base), po, pw, workspace.numel(),
+                                 _stream_handle(stream)), "decode_rope")
     return out
 
 

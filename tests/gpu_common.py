@@ -74,9 +74,21 @@ def run_decode(inp: Inputs, plan, pool: torch.Tensor, q: np.ndarray = None) -> n
     return out.cpu().numpy().astype(np.float64)
 
 
+def seq_latents(inp: Inputs, b: int):
+    """Key and value latents [T_b, .] of sequence b as the oracle sees them:
+    the seeded pre-filled latents, then (sequence 0) the oracle's append."""
+    wl = inp.wl
+    Zk = inp.Zk_prefill[b]
+    Zv = inp.Zv_prefill[b]
+    if b == 0 and wl.append_tokens:
+        Zka, Zva = oappend.latents(inp.x, inp.L_keys, inp.L_value, wl.dtype)
+        Zk = np.concatenate([Zk, Zka.astype(np.float32)])
+        Zv = np.concatenate([Zv, Zva.astype(np.float32)])
+    return Zk, Zv
+
+
 def oracle_rows(inp: Inputs, pairs, q: np.ndarray = None) -> dict:
     """Oracle outputs of (sequence, head) pairs, from the seeded latents."""
-    wl = inp.wl
     bk = book_for(wl)
     q = inp.q if q is None else q
     res = {}
@@ -84,12 +96,7 @@ def oracle_rows(inp: Inputs, pairs, q: np.ndarray = None) -> dict:
     for b, h in pairs:
         by_b.setdefault(b, []).append(h)
     for b, heads in sorted(by_b.items()):
-        Zk = inp.Zk_prefill[b]
-        Zv = inp.Zv_prefill[b]
-        if b == 0 and wl.append_tokens:
-            Zka, Zva = oappend.latents(inp.x, inp.L_keys, inp.L_value, wl.dtype)
-            Zk = np.concatenate([Zk, Zka.astype(np.float32)])
-            Zv = np.concatenate([Zv, Zva.astype(np.float32)])
+        Zk, Zv = seq_latents(inp, b)
         for h in heads:
             res[(b, h)] = oattn.decode_head(q[b, h], Zk, Zv, inp.R_blocks, inp.R_value, bk, h,
                                             chunk=8192)

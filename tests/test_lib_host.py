@@ -216,3 +216,42 @@ def test_group_order_cuts_the_smallest_group():
     assert g["key_chunk_loads"] == 30 and g["decode_ring"] == 16
     # the portable path reports none
     assert _plan(make_workload("tiny_mha_f32")).geometry["key_chunk_loads"] == 0
+
+
+@pytest.mark.skipif(torch.cuda.is_available(), reason="raw fake pointers are only passed on a host without a GPU")
+def test_rope_call_validation_never_launches(lib):
+    from paper_2607_24331_amd import Plan
+    A = 1 << 20
+    n = ctypes.c_size_t()
+    # the rotary decode runs on the bf16 MFMA path only, one query a sequence
+    p32 = _plan(make_workload("tiny_mha_f32"))
+    assert lib.dckv_rope_workspace_bytes(p32.handle, 1, 256, ctypes.byref(n)) == capi.DCKV_EINVAL
+    assert "MFMA" in lib.dckv_last_error().decode()
+    wl = make_workload("gqa8b_b4_t32k")
+    pq = Plan(wl.hidden, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_of_kv,
+              wl.group_rank, wl.value_rank, wl.dtype, 0, queries_per_seq=4)
+    assert lib.dckv_rope_workspace_bytes(pq.handle, 1, 256, ctypes.byref(n)) == capi.DCKV_EINVAL
+    p = _plan(wl)
+    assert lib.dckv_rope_workspace_bytes(p.handle, 4, 32768, ctypes.byref(n)) == capi.DCKV_OK
+    need = n.value
+    assert need > 0
+    assert lib.dckv_rope_workspace_bytes(p.handle, 1, 1024, ctypes.byref(n)) == capi.DCKV_OK
+    assert 0 < n.value < need
+    args = [p.handle, A, 4, A, 4, A, 512, A, 32768, A, A, 10000.0, A, A, need, None]
+
+    def call(**kw):
+        a = list(args)
+        idx = {"q": 1, "batch": 2, "num_pages": 4, "max_pages": 6, "max_context": 8,
+               "base": 11, "out": 12, "ws": 13, "ws_bytes": 14}
+        for k, v in kw.items():
+            a[idx[k]] = v
+        return lib.dckv_decode_rope(*a)
+    for bad in (1.0, 0.5, float("nan"), float("inf"), -3.0):
+        assert call(base=bad) == capi.DCKV_EINVAL
+    assert call(q=None) == capi.DCKV_EINVAL
+    assert call(max_context=512 * 64 + 1) == capi.DCKV_EINVAL
+    assert call(out=A + 4) == capi.DCKV_EALIGN
+    assert call(ws=A + 16) == capi.DCKV_EALIGN
+    assert call(ws_bytes=need - 1) == capi.DCKV_EWORKSPACE
+    assert call(batch=0) == capi.DCKV_OK
+    assert lib.dckv_decode_rope(None, *args[1:]) == capi.DCKV_EINVAL
