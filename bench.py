@@ -51,6 +51,10 @@ def parse():
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one device copy of this many MiB before timing (a known-size "
                          "kernel for scaling hardware traffic counters)")
+    ap.add_argument("--rope", type=float, default=None, metavar="BASE",
+                    help="time the rotary decode (keys rebuilt per token and turned by their "
+                         "position, planes at angle pos * BASE^(-2i/d_h)) instead of the "
+                         "position-free one")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle sample")
     ap.add_argument("--offline", choices=["cka", "calib"], default=None,
@@ -62,6 +66,7 @@ def parse():
 
 
 MFMA_F32_PEAK_TFLOPS = 157.3
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 
 def main_offline(args, torch):
@@ -254,7 +259,7 @@ def measured_traffic(wl, launch, Q=1):
         return None
 
 
-def cpu_baseline(wl, budget_s, Q=1, with_append=True):
+def cpu_baseline(wl, budget_s, Q=1, with_append=True, rope_base=None):
     """The oracle, as it stands, on a bounded sample of the same workload:
     the append of all new tokens plus whole-context decode of as many heads
     as fit the time budget; the step time is extrapolated to every (sequence,
@@ -262,6 +267,7 @@ def cpu_baseline(wl, budget_s, Q=1, with_append=True):
     import numpy as np
     from oracle import append as oappend
     from oracle import attention as oattn
+    from oracle import rope as orope
     from oracle.bookkeeping import book_for
     from workloads.inputs import make_factors
     try:
@@ -287,7 +293,10 @@ def cpu_baseline(wl, budget_s, Q=1, with_append=True):
     heads_done, t_dec = 0, 0.0
     for h in range(wl.num_q_heads):
         t0 = time.perf_counter()
-        oattn.decode_head(q[b, h], Zk, Zv, R_blocks, R_value, bk, h, chunk=16384)
+        if rope_base is None:
+            oattn.decode_head(q[b, h], Zk, Zv, R_blocks, R_value, bk, h, chunk=16384)
+        else:
+            orope.decode_head(q[b, h], Zk, Zv, R_blocks, R_value, bk, h, rope_base, chunk=16384)
         t_dec += time.perf_counter() - t0
         heads_done += 1
         if t_dec + t_app >= budget_s:
@@ -302,7 +311,9 @@ def cpu_baseline(wl, budget_s, Q=1, with_append=True):
         "cores": int(threads),
         "kind": "oracle",
         "sample": ((f"oracle append of {wl.append_tokens} tokens ({t_app:.2f} s) + "
-                    if wl.append_tokens and with_append else "") + "fp64 decode of "
+                    if wl.append_tokens and with_append else "")
+                   + ("fp64 rotary decode of " if rope_base is not None else "fp64 decode of ")
+                   + 
                    f"{heads_done} of {rows} (sequence, query, head) rows at {T} context tokens "
                    f"({t_dec:.2f} s), extrapolated to the full step ({step_s:.1f} s)"),
     }
@@ -420,7 +431,7 @@ def main():
         sys.exit(2)
     import torch
     sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
-    from paper_2607_24331_amd import Plan, decode, latent_append
+    from paper_2607_24331_amd import Plan, decode, decode_rope, latent_append
     from workloads import make_workload
 
     if args.offline:
@@ -437,15 +448,27 @@ def main():
     max_ctx = max(wl.seq_lens)
     split_used = plan.split_tokens or _auto_split(plan, wl, max_ctx)
     out = torch.empty(tuple(inp["q"].shape), dtype=torch.float32, device="cuda")
-    ws = plan.new_workspace(wl.batch, max_ctx)
+    rope = args.rope is not None
+    if rope:
+        if Q != 1 or not mfma:
+            sys.exit("bench.py: --rope runs one query a sequence on the bf16 MFMA path")
+        split_used = min(split_used, 1024)            # the rotary decode's split cap
+        ws = torch.empty(max(256, plan.rope_workspace_bytes(wl.batch, max_ctx)), dtype=torch.uint8,
+                         device="cuda")
+    else:
+        ws = plan.new_workspace(wl.batch, max_ctx)
 
     append = bool(wl.append_tokens) and not args.decode_only
 
     def step():
         if append:
             latent_append(plan, inp["x"], inp["L_keys"], inp["L_value"], inp["slot"], inp["pool"])
-        decode(plan, inp["q"], inp["pool"], inp["page_table"], inp["seq_lens"], max_ctx,
-               inp["R_keys"], inp["R_value"], out=out, workspace=ws)
+        if rope:
+            decode_rope(plan, inp["q"], inp["pool"], inp["page_table"], inp["seq_lens"], max_ctx,
+                        inp["R_keys"], inp["R_value"], rope_base=args.rope, out=out, workspace=ws)
+        else:
+            decode(plan, inp["q"], inp["pool"], inp["page_table"], inp["seq_lens"], max_ctx,
+                   inp["R_keys"], inp["R_value"], out=out, workspace=ws)
 
     if args.copy_calibration_mib:
         n = args.copy_calibration_mib * (1 << 20) // 4
@@ -484,7 +507,8 @@ def main():
     ms_total = t_start.elapsed_time(t_end)
     ms_step = ms_total / K
     kern_ms = sum(a.elapsed_time(b) for a, b in ev.values()) / len(ev)
-    print(f"[bench] timed {K} steps: {ms_step:.4f} ms/step, split kernel {kern_ms:.4f} ms "
+    print(f"[bench] timed {K} steps: {ms_step:.4f} ms/step, "
+          f"{'key-rebuild' if rope else 'split'} kernel {kern_ms:.4f} ms "
           f"(HIP events on {len(ev)} of the {K} steps)",
           file=sys.stderr, flush=True)
 
@@ -540,9 +564,26 @@ def main():
             "launch": launch,
         },
     }
+    if rope:
+        # the key rebuild is the dominant kernel: r_g * d_h MACs a token and KV head
+        kv_ranks = sum(wl.group_rank[wl.group_of_kv[kv]] for kv in range(wl.num_kv_heads))
+        flops = 2.0 * wl.head_dim * kv_ranks * sum(wl.seq_lens)
+        tf = flops / (kern_ms * 1e-3) / 1e12
+        rec["metric"] = ("compressed-KV rotary decode attention tokens/s "
+                         "(key-rebuild MFMA TFLOP/s in roofline)")
+        rec["config"]["rope_base"] = args.rope
+        rec["config"]["split_tokens"] = split_used
+        rec["roofline"] = {
+            "kernel": "rotary key rebuild + scores + split softmax (rope_scores, bf16 MFMA)",
+            "bound": "mfma", "achieved": tf, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": tf / MFMA_BF16_PEAK_TFLOPS, "traffic": None, "kernel_ms": kern_ms,
+            "kernel_launches_timed": len(ev), "flops_per_launch": flops,
+            "key_latent_bytes_per_launch": sum(wl.seq_lens) * wl.key_rank_total * wl.elem_bytes,
+            "launch": f"split_tokens={split_used} work-groups=batch*splits*kv_heads",
+        }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
-        rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, Q, append)
+        rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, Q, append, args.rope)
     print(json.dumps(rec), flush=True)
 
 

@@ -72,6 +72,32 @@ def test_rope_small_all_rows(name, base):
     assert max(errs) <= TOL_REL_ROW
 
 
+def _wide_inputs():
+    # a group of rank 470 spans 15 key chunks: wider than the resident-factor
+    # kernel holds at d_h = 128, so the general (per-chunk staging) kernel runs
+    from test_gpu_parity import _groups
+    from workloads.configs import custom_workload
+    lens = (1500, 70, 640)
+    wl = custom_workload(name="wide_group", seed=321, hidden=1024, num_q_heads=16, num_kv_heads=8,
+                         head_dim=128, group_of_kv=_groups((5, 3), 11), group_rank=(470, 96),
+                         value_rank=256, dtype="bf16", batch=len(lens), seq_lens=lens,
+                         prefill_lens=lens, factor_scheme="orthonormal", permute_pages=True)
+    return wl, make_inputs(wl)
+
+
+@pytest.mark.parametrize("split", [512, 1024])
+def test_rope_wide_group_general_kernel(split):
+    wl, inp = _wide_inputs()
+    plan = plan_for(wl, split)
+    print(f"[rope] wide_group split {split}", flush=True)
+    pool = gpu_pool_with_append(inp, plan)
+    out = _run(inp, plan, pool, 10000.0)
+    ref = _rope_rows(inp, [(b, h) for b in range(wl.batch) for h in range(wl.num_q_heads)], 10000.0)
+    errs = [row_rel_err(out[b, h], o) for (b, h), o in ref.items()]
+    print(f"[rope] wide_group/{split}: max row rel err {max(errs):.3e} over {len(errs)} rows", flush=True)
+    assert max(errs) <= TOL_REL_ROW
+
+
 def test_rope_differs_from_position_free_and_is_reproducible():
     from paper_2607_24331_amd import decode
     wl, inp, split = _small_inputs("gqa_uneven")
