@@ -36,12 +36,14 @@ constexpr int kRopeMaxSplit = 1024;      // context tokens a split
 constexpr int kDepth = 4;                // key chunks in flight ahead of the MFMAs
 constexpr int kRsrcWord3 = 0x00020000;   // raw buffer descriptor word 3 (gfx9 family)
 constexpr int kNonTemporal = 2;
+constexpr int kOutOfRange = 0x40000000;   // byte offset beyond any page: the load reads zero
 constexpr double kInv2Pi = 0.15915494309189533577;
 constexpr int kResWaves = 8;              // waves of the resident-factor kernel
 constexpr int kResFacElems = 57344;       // its LDS factor blocks: 112 KB of bf16
 constexpr int kResMaxPages = 128;         // pages a work-group of it
 constexpr int kResTargetGroups = 1024;    // work-groups it aims for (four a compute unit)
 constexpr int kResScores = 8192;          // scores of a work-group's range in LDS
+constexpr int kResDepth = 3;              // its key chunks in flight a wave
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -113,25 +115,34 @@ __global__ __launch_bounds__(256) void rope_factors(const bf16* __restrict__ Rk,
 // token's angle, then the key is dotted with each query (qr: turned and
 // scaled, rows of D floats); lane lq == 0 writes the score of token 16 n + lr
 // to sc[hh * stride + off + 16 n + lr], or -inf past nval or on an empty
-// page.
+// page.  The angle of a plane is formed once a page (token pos0 + lr) and
+// stepped to the lane's other tokens, 16 apart, by the turn through 16
+// theta_a (cs16[a]: its cosine and sine).
 template <int DT>
 __device__ __forceinline__ void page_scores(floatx4 (&acc)[DT][4], int pos0, int nval, bool pvalid,
-                                            const double* omega, const float* qr, int qpk,
-                                            float* sc, int stride, int off, int lane) {
+                                            const double* omega, const float2* cs16,
+                                            const float* qr, int qpk, float* sc, int stride,
+                                            int off, int lane) {
   constexpr int D = 16 * DT, HALF = DT / 2;
   const int lr = lane & 15, lq = lane >> 4;
 #pragma unroll
   for (int it = 0; it < HALF; ++it)
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      const double om = omega[16 * it + 4 * lq + v];
+      const int a = 16 * it + 4 * lq + v;
+      float cs, sn;
+      turn(pos0 + lr, omega[a], cs, sn);
+      const float2 st = cs16[a];
 #pragma unroll
       for (int n = 0; n < 4; ++n) {
-        float cs, sn;
-        turn(pos0 + 16 * n + lr, om, cs, sn);
         const float ka = acc[it][n][v], kb = acc[it + HALF][n][v];
         acc[it][n][v] = ka * cs - kb * sn;
         acc[it + HALF][n][v] = kb * cs + ka * sn;
+        if (n < 3) {
+          const float c2 = cs * st.x - sn * st.y;
+          sn = sn * st.x + cs * st.y;
+          cs = c2;
+        }
       }
     }
   for (int hh = 0; hh < qpk; ++hh) {
@@ -261,6 +272,7 @@ __global__ __launch_bounds__(256, 1) void rope_scores(
   __shared__ __align__(16) float qr[kMaxQpk][D];
   __shared__ __align__(16) float sc[kMaxQpk][kRopeMaxSplit];
   __shared__ double omega[D / 2];
+  __shared__ float2 cs16[D / 2];
   __shared__ int pids[kRopeMaxSplit / 64];
   __shared__ float redm[4], redl[4];
 
@@ -292,7 +304,13 @@ __global__ __launch_bounds__(256, 1) void rope_scores(
   const int kvalid_last = min(8, max(0, RK - (32 * kc_last + 8 * lq)));
 
   // ---- prologue: plane frequencies, the split's pages, turned queries
-  if (tid < D / 2) omega[tid] = exp2(-(2.0 * tid / D) * log2_base) * kInv2Pi;
+  if (tid < D / 2) {
+    const double om = exp2(-(2.0 * tid / D) * log2_base) * kInv2Pi;
+    omega[tid] = om;
+    float c16, s16;
+    turn(16, om, c16, s16);
+    cs16[tid] = make_float2(c16, s16);
+  }
   if (tid < np) {
     const int pg = page_table[int64_t(b) * max_pages + (t0 >> 6) + tid];
     pids[tid] = (pg >= 0 && pg < num_pages) ? pg : -1;
@@ -407,7 +425,7 @@ __global__ __launch_bounds__(256, 1) void rope_scores(
           const int pg = 4 * round + w;
           if (pg < np)
             page_scores<DT>(acc, t0 + 64 * pg, min(64, (t1 - t0) - 64 * pg), pids[pg] >= 0, omega,
-                            &qr[0][0], qpk, &sc[0][0], kRopeMaxSplit, 64 * pg, lane);
+                            cs16, &qr[0][0], qpk, &sc[0][0], kRopeMaxSplit, 64 * pg, lane);
 #pragma unroll
           for (int i = 0; i < DT; ++i)
 #pragma unroll
@@ -446,13 +464,14 @@ __global__ __launch_bounds__(512, 1) void rope_scores_res(
     int max_context, int split_tokens, int n_split, int spw, int n_ranges, int n_work,
     const bf16* __restrict__ rt, int RK, int64_t page_elems, double log2_base, float scale,
     int n_slices, bf16* __restrict__ pbuf, float* __restrict__ part_ml, RopeTables tb) {
-  constexpr int W = kResWaves, D = 16 * DT, P = kDepth;
+  constexpr int W = kResWaves, D = 16 * DT, P = kResDepth;
   extern __shared__ __align__(16) unsigned char smem[];
   bf16* fac = reinterpret_cast<bf16*>(smem);                                // [nch][DT][512]
   float* sc = reinterpret_cast<float*>(smem + size_t(kResFacElems) * 2);    // [qpk][spw * L]
   float* qr = sc + kResScores;                                              // [kMaxQpk][D]
   double* omega = reinterpret_cast<double*>(qr + kMaxQpk * D);              // [D/2]
-  int* pids = reinterpret_cast<int*>(omega + D / 2);                        // [kResMaxPages]
+  float2* cs16 = reinterpret_cast<float2*>(omega + D / 2);                  // [D/2]
+  int* pids = reinterpret_cast<int*>(cs16 + D / 2);                         // [kResMaxPages]
 
   // XCD-aware order as in rope_scores: the KV heads of one (sequence, range)
   // are consecutive items on one XCD
@@ -487,7 +506,13 @@ __global__ __launch_bounds__(512, 1) void rope_scores_res(
 
   // ---- prologue: frequencies and pages; then the turned queries and the
   // head's factor blocks (eight 16-byte loads in flight a thread)
-  if (tid < D / 2) omega[tid] = exp2(-(2.0 * tid / D) * log2_base) * kInv2Pi;
+  if (tid < D / 2) {
+    const double om = exp2(-(2.0 * tid / D) * log2_base) * kInv2Pi;
+    omega[tid] = om;
+    float c16, s16;
+    turn(16, om, c16, s16);
+    cs16[tid] = make_float2(c16, s16);
+  }
   if (tid < npw) {
     const int pg = page_table[int64_t(b) * max_pages + (t0w >> 6) + tid];
     pids[tid] = (pg >= 0 && pg < num_pages) ? pg : -1;
@@ -519,8 +544,13 @@ __global__ __launch_bounds__(512, 1) void rope_scores_res(
   __syncthreads();
 
   // ---- steps: (split, round, chunk); this wave's page of a round is
-  // round * W + w of the split
-  const int total = nsp * rps * nch;
+  // round * W + w of the split.  A round is padded to nchp = a multiple of P
+  // chunks, so a loop body is P chunks of one round and the page's scores
+  // follow the body that ends the round: the loads of every step are issued
+  // on every path (a padding chunk's load is out of range and reads zero)
+  // and each wait is for its own ring slot only.
+  const int nchp = (nch + P - 1) / P * P;
+  const int total = nsp * rps * nchp;
   const int page_bytes = int(page_elems * 2);
   const int lane_key = 2 * (lr * 32 + 8 * lq);
   auto page_rsrc = [&](int sp, int r) {
@@ -533,7 +563,7 @@ __global__ __launch_bounds__(512, 1) void rope_scores_res(
                                              kRsrcWord3);
   };
   auto load_key = [&](u32x4 (&z)[4], __amdgpu_buffer_rsrc_t rs, int c) {
-    const int o = 2 * 2048 * (c_lo + c) + lane_key;
+    const int o = c < nch ? 2 * 2048 * (c_lo + c) + lane_key : kOutOfRange;
 #pragma unroll
     for (int n = 0; n < 4; ++n)
       z[n] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, o + 2 * 512 * n, 0, kNonTemporal));
@@ -542,7 +572,7 @@ __global__ __launch_bounds__(512, 1) void rope_scores_res(
   int is_c = 0, is_r = 0, is_s = 0;
   __amdgpu_buffer_rsrc_t is_rs = page_rsrc(0, 0);
   auto advance_issue = [&]() {
-    if (++is_c == nch) {
+    if (++is_c == nchp) {
       is_c = 0;
       if (++is_r == rps) {
         is_r = 0;
@@ -563,51 +593,47 @@ __global__ __launch_bounds__(512, 1) void rope_scores_res(
 #pragma unroll
     for (int n = 0; n < 4; ++n) acc[i][n] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  int c = 0, r = 0, sp = 0;                        // consume position
+  int c0 = 0, r = 0, sp = 0;                       // consume position: first chunk of the body
   for (int s0 = 0; s0 < total; s0 += P) {
 #pragma unroll
     for (int s = 0; s < P; ++s) {
-      if (s0 + s < total) {                        // uniform over the work-group
-        u32x4 z[4];
-        {
-          u32x4 zn[4];
-          load_key(zn, is_rs, is_c);               // past the range: an empty page, reads zero
-#pragma unroll
-          for (int n = 0; n < 4; ++n) {
-            z[n] = zr[s][n];
-            zr[s][n] = zn[n];
-          }
-          advance_issue();
-        }
+      const int c = c0 + s;
+      if (c < nch) {                               // a real chunk (uniform)
         if (c_lo + c == kc_last) {
 #pragma unroll
-          for (int n = 0; n < 4; ++n) z[n] = keep_first(z[n], kvalid_last);
+          for (int n = 0; n < 4; ++n) zr[s][n] = keep_first(zr[s][n], kvalid_last);
         }
         const bf16* A = fac + c * (DT * 512) + lane * 8;
+        u32x4 a[DT];                               // the step's factor fragments, all in flight
 #pragma unroll
-        for (int it = 0; it < DT; ++it) {
-          const u32x4 a = *reinterpret_cast<const u32x4*>(A + it * 512);
+        for (int it = 0; it < DT; ++it) a[it] = *reinterpret_cast<const u32x4*>(A + it * 512);
 #pragma unroll
-          for (int n = 0; n < 4; ++n) acc[it][n] = mfma(a, z[n], acc[it][n]);
-        }
-        if (c == nch - 1) {                        // the wave's page of the round is rebuilt
-          const int pgi = r * W + w;
-          const int pos0 = t0w + sp * L + 64 * pgi;
-          if (pgi < pps && pos0 < t1w)
-            page_scores<DT>(acc, pos0, min(64, t1w - pos0), pids[sp * pps + pgi] >= 0, omega, qr,
-                            qpk, sc, spw * L, sp * L + 64 * pgi, lane);
+        for (int it = 0; it < DT; ++it)
 #pragma unroll
-          for (int i = 0; i < DT; ++i)
+          for (int n = 0; n < 4; ++n) acc[it][n] = mfma(a[it], zr[s][n], acc[it][n]);
+        __builtin_amdgcn_sched_group_barrier(0x100, DT, 0);      // the DT LDS reads first,
+        __builtin_amdgcn_sched_group_barrier(0x008, 4 * DT, 0);  // then the step's MFMAs
+      }
+      // the slot is used in place and reloaded after its MFMAs: no register
+      // copy ties a wait to the loads just issued
+      load_key(zr[s], is_rs, is_c);                // past the range: an empty page, reads zero
+      advance_issue();
+    }
+    c0 += P;
+    if (c0 == nchp) {                              // the wave's page of the round is rebuilt
+      const int pgi = r * W + w;
+      const int pos0 = t0w + sp * L + 64 * pgi;
+      if (pgi < pps && pos0 < t1w)
+        page_scores<DT>(acc, pos0, min(64, t1w - pos0), pids[sp * pps + pgi] >= 0, omega, cs16,
+                        qr, qpk, sc, spw * L, sp * L + 64 * pgi, lane);
 #pragma unroll
-            for (int n = 0; n < 4; ++n) acc[i][n] = floatx4{0.f, 0.f, 0.f, 0.f};
-          c = 0;
-          if (++r == rps) {
-            r = 0;
-            ++sp;
-          }
-        } else {
-          ++c;
-        }
+      for (int i = 0; i < DT; ++i)
+#pragma unroll
+        for (int n = 0; n < 4; ++n) acc[i][n] = floatx4{0.f, 0.f, 0.f, 0.f};
+      c0 = 0;
+      if (++r == rps) {
+        r = 0;
+        ++sp;
       }
     }
   }
@@ -663,7 +689,7 @@ hipError_t launch_rope_factors(const dckv_plan& p, const void* R_keys, void* rt,
 
 size_t rope_res_lds_bytes(int dh) {
   return size_t(kResFacElems) * 2 + size_t(kResScores) * 4 + size_t(kMaxQpk) * dh * 4 +
-         size_t(dh / 2) * 8 + kResMaxPages * 4;
+         size_t(dh / 2) * 16 + kResMaxPages * 4;
 }
 
 hipError_t launch_rope_scores(const dckv_plan& p, const DecodeShape& sh, const float* q,
