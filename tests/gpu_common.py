@@ -89,7 +89,7 @@ def seq_latents(inp: Inputs, b: int):
 
 def oracle_rows(inp: Inputs, pairs, q: np.ndarray = None) -> dict:
     """Oracle outputs of (sequence, head) pairs, from the seeded latents."""
-    bk = book_for(wl)
+    bk = book_for(inp.wl)
     q = inp.q if q is None else q
     res = {}
     by_b = {}
