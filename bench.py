@@ -220,27 +220,31 @@ def algorithmic_bytes(wl):
 
 KERNEL_SOURCES = ("paper_2607_24331_amd/csrc/decode_mfma.hip", "paper_2607_24331_amd/csrc/plan.cpp",
                   "paper_2607_24331_amd/csrc/internal.h")
+ROPE_KERNEL_SOURCES = ("paper_2607_24331_amd/csrc/rope.hip", "paper_2607_24331_amd/csrc/plan.cpp",
+                       "paper_2607_24331_amd/csrc/internal.h")
 
 
-def kernel_sources_sha256():
+def kernel_sources_sha256(sources=KERNEL_SOURCES):
     import hashlib
     h = hashlib.sha256()
     root = os.path.dirname(os.path.abspath(__file__))
-    for rel in KERNEL_SOURCES:
+    for rel in sources:
         with open(os.path.join(root, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
 
 
-def measured_traffic(wl, launch, Q=1):
-    """HBM bytes per launch of the split kernel from the committed counter
-    summary (FETCH_SIZE and WRITE_SIZE, each scaled by the same counter's
-    reading for a plain device copy of known size), or None when there is
-    no summary for this workload and launch shape, or the kernel sources
-    changed since the counters were taken."""
+def measured_traffic(wl, launch, Q=1, kernel="split_mfma"):
+    """HBM bytes per launch of the dominant kernel (the split kernel, or the
+    rotary key rebuild) from the committed counter summary (FETCH_SIZE and
+    WRITE_SIZE, each scaled by the same counter's reading for a plain device
+    copy of known size), or None when there is no summary for this workload
+    and launch shape, or the kernel sources changed since the counters were
+    taken."""
     root = os.path.dirname(os.path.abspath(__file__))
     tag = wl.name if Q == 1 else f"{wl.name}_q{Q}"
-    path = os.path.join(root, "profiles", f"split_mfma_{tag}_counters.md")
+    path = os.path.join(root, "profiles", f"{kernel}_{tag}_counters.md")
+    sources = ROPE_KERNEL_SOURCES if kernel == "rope_scores" else KERNEL_SOURCES
     if not os.path.exists(path):
         return None
     keys = {}
@@ -251,7 +255,7 @@ def measured_traffic(wl, launch, Q=1):
                 k, v = line.split(":", 1)
                 keys[k.strip()] = v.strip()
     if (keys.get("workload") != wl.name or keys.get("launch") != launch
-            or keys.get("kernel_sources_sha256") != kernel_sources_sha256()):
+            or keys.get("kernel_sources_sha256") != kernel_sources_sha256(sources)):
         return None
     try:
         return int(keys["traffic_bytes_per_launch"])
@@ -574,12 +578,14 @@ def main():
         rec["config"]["rope_base"] = args.rope
         rec["config"]["split_tokens"] = split_used
         rec["roofline"] = {
-            "kernel": "rotary key rebuild + scores + split softmax (rope_scores, bf16 MFMA)",
+            "kernel": "rotary key rebuild + scores + split softmax (rope_scores_res, bf16 MFMA)",
             "bound": "mfma", "achieved": tf, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-            "frac": tf / MFMA_BF16_PEAK_TFLOPS, "traffic": None, "kernel_ms": kern_ms,
+            "frac": tf / MFMA_BF16_PEAK_TFLOPS,
+            "traffic": measured_traffic(wl, f"split_tokens={split_used} rope", 1, "rope_scores"),
+            "kernel_ms": kern_ms,
             "kernel_launches_timed": len(ev), "flops_per_launch": flops,
             "key_latent_bytes_per_launch": sum(wl.seq_lens) * wl.key_rank_total * wl.elem_bytes,
-            "launch": f"split_tokens={split_used} work-groups=batch*splits*kv_heads",
+            "launch": f"split_tokens={split_used} rope",
         }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)

@@ -176,6 +176,7 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
   constexpr int NV = ((2 * MTW + VR - 1) / VR) * VR;   // value items a page (padded)
   static_assert(KR % 2 == 0 && KR % MPW == 0 && VR % 2 == 0, "blocks hold whole chunks and k-steps");
   static_assert(!PW || KR == VR, "the weighted value pass streams values only");
+  static_assert(!PW || NV == 2 * MTW, "the weighted value pass has no padding items");
   extern __shared__ __align__(16) unsigned char smem[];
 
   const int J = mt.n_slices;
@@ -296,6 +297,7 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
     // of it is the 512-element run starting at m * 512.  Value tile u (16
     // ranks) holds the two 32-token halves as 512-element runs from u * 1024.
     r.base = r.kind == 0 ? 2 * (512 * mb_w)
+           : PW          ? 2 * (int(value_base) + 1024 * mt0_w)
                          : 2 * (int(value_base) + 1024 * (mt0_w + (r.idx0 - NK) / 2));
     return r;
   };
@@ -310,10 +312,19 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
       const bool ok = (i < nk_real) & (32 * c + 8 * lq < RK);     // no short-circuit branches
       off = ok ? o : kOutOfRange;
     } else if (pb.kind == 1) {
-      const int mtl = (pb.idx0 - NK + s) >> 1;
-      const int o = pb.base + 2 * (1024 * (s >> 1) + 512 * (s & 1)) + lane_val;
-      const bool ok = (mtl < mcnt_w) & (16 * (mt0_w + mtl) + lr < rv) & (32 * (s & 1) + 8 * lq < pb.nval);
-      off = ok ? o : kOutOfRange;
+      if constexpr (PW) {
+        // half-major: item j of the page is tile j % MTW of token half j / MTW
+        const int j = pb.idx0 - NK + s;
+        const int mtl = j % MTW, ks = j / MTW;
+        const int o = pb.base + 2 * (1024 * mtl + 512 * ks) + lane_val;
+        const bool ok = (mtl < mcnt_w) & (16 * (mt0_w + mtl) + lr < rv) & (32 * ks + 8 * lq < pb.nval);
+        off = ok ? o : kOutOfRange;
+      } else {
+        const int mtl = (pb.idx0 - NK + s) >> 1;
+        const int o = pb.base + 2 * (1024 * (s >> 1) + 512 * (s & 1)) + lane_val;
+        const bool ok = (mtl < mcnt_w) & (16 * (mt0_w + mtl) + lr < rv) & (32 * (s & 1) + 8 * lq < pb.nval);
+        off = ok ? o : kOutOfRange;
+      }
     }
     return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(pb.rsrc, off, 0, kNonTemporal));
   };
@@ -326,16 +337,16 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
   }
 
   if constexpr (PW) {
-    // ---- the split's weights into LDS, eight loads in flight a thread;
+    // ---- the split's weights into LDS, four loads in flight a thread;
     // padding slots (no query head) get zero weights
     const bf16* src = pw + (int64_t(b * J + slice) * n_split + split) * NH * split_tokens;
     const int vrow = split_tokens / 8, nvec = NH * vrow;
-    for (int base = tid; base < nvec; base += 8 * W * 64) {
-      u32x4 v[8];
+    for (int base = tid; base < nvec; base += 4 * W * 64) {
+      u32x4 v[4];
 #pragma unroll
-      for (int k = 0; k < 8; ++k) v[k] = *reinterpret_cast<const u32x4*>(src + 8 * min(base + k * W * 64, nvec - 1));
+      for (int k = 0; k < 4; ++k) v[k] = *reinterpret_cast<const u32x4*>(src + 8 * min(base + k * W * 64, nvec - 1));
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
+      for (int k = 0; k < 4; ++k) {
         const int idx = base + k * W * 64;
         if (idx < nvec) {
           const int slot = idx / vrow, col = idx - slot * vrow;
@@ -392,10 +403,8 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
     u32x4 pB[NT][2];
     if constexpr (PW) {                   // weights ready in LDS: no keys, no softmax
 #pragma unroll
-      for (int n = 0; n < NT; ++n)
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
-          pB[n][ks] = *reinterpret_cast<const u32x4*>(p_all + (16 * n + lr) * pst + 64 * page + 32 * ks + 8 * lq);
+      for (int n = 0; n < NT; ++n)        // the first token half's (the second's at mid-page)
+        pB[n][0] = *reinterpret_cast<const u32x4*>(p_all + (16 * n + lr) * pst + 64 * page + 8 * lq);
     } else {
 
     // ---- scores: MPW M-tiles (16 tokens each) of this wave's N-tile
@@ -541,7 +550,14 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
 #pragma unroll
       for (int s = 0; s < VR; ++s) {
         const int i = vb + s;
-        const int mtl = i >> 1, ks = i & 1;
+        const int mtl = PW ? i % MTW : i >> 1, ks = PW ? i / MTW : i & 1;
+        if constexpr (PW) {
+          if (i == MTW) {
+#pragma unroll
+            for (int n = 0; n < NT; ++n)
+              pB[n][1] = *reinterpret_cast<const u32x4*>(p_all + (16 * n + lr) * pst + 64 * page + 32 + 8 * lq);
+          }
+        }
         u32x4 a = ring[s];
         if (nval < 64) a = keep_first(a, ks ? keep1 : keep0);
         if (mtl < MTW) {

@@ -9,16 +9,18 @@
 // rope_factors: R_{g,h}^T of every KV head copied into 16 x 32 bf16 blocks in
 //   MFMA A-operand order, one block per (32-column key chunk meeting the
 //   group's columns, 16 rows of d_h), zero outside the group's columns.
-// rope_scores: one 256-thread work-group (four waves) per (sequence, context
-//   split, KV head).  The four waves take four pages at a time; per 32-column
-//   key chunk they share the chunk's factor blocks, staged once in LDS, and
-//   each forms K^T[dim][tok] += R^T[dim][k] Z[tok][k] for its page on MFMA
-//   16x16x32 bf16 (exact bf16 products, fp32 sums).  A page done, each plane
-//   (i, i + d_h/2) is turned by the token's angle and the key is dotted with
-//   the KV head's turned, scaled queries.  At the split's end the work-group
-//   writes, per query head, the split maximum m, the weights 2^(s - m)
-//   rounded to bf16, and their sum l: the split's partial softmax, in the
-//   form the value pass and the merge of the position-free decode take.
+// rope_scores_res (groups whose factor blocks fit LDS) and rope_scores (any
+//   group): per (sequence, context splits, KV head) a work-group's waves
+//   each take one 64-token page at a time and form K^T[dim][tok] +=
+//   R^T[dim][k] Z[tok][k] over the group's key chunks on MFMA 16x16x32 bf16
+//   (exact bf16 products, fp32 sums), the factor blocks read from LDS.  A
+//   page done, each plane (i, i + d_h/2) is turned by the token's angle and
+//   the key is dotted with the KV head's turned, scaled queries.  Per split
+//   the work-group writes, per query head, the split maximum m, the weights
+//   2^(s - m) rounded to bf16, and their sum l: the split's partial softmax,
+//   in the form the value pass and the merge of the position-free decode
+//   take.  rope_scores_res keeps the head's blocks resident for its whole
+//   range of splits; rope_scores stages one chunk's blocks a step.
 #include <cmath>
 
 #include "device.h"
@@ -453,7 +455,7 @@ __global__ __launch_bounds__(256, 1) void rope_scores(
 // and dot products overlap the other's MFMAs) per (sequence, range of spw
 // context splits, KV head).  The head's blocks are staged in LDS once; the
 // waves then run through the range's pages independently, eight pages a
-// round, each wave with its own page and its own ring of key loads kDepth
+// round, each wave with its own page and its own ring of key loads kResDepth
 // chunks ahead.  Scores of the whole range stay in LDS (qpk * spw * L <=
 // kResScores floats); at the end each wave takes whole splits for their
 // softmax, so the waves meet only twice: after staging and before the tail.
