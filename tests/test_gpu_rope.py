@@ -128,7 +128,7 @@ def test_rope_split_lengths_agree():
 
 
 @pytest.mark.parametrize("name, n_rows", [("gqa8b_b4_t32k", 6), ("mha_long_t128k", 4),
-                                          ("mha7b_b8_t4k", 6)])
+                                          ("mha7b_b8_t4k", 6), ("mha_ragged_b64", 12)])
 def test_rope_full_size_sampled_rows(name, n_rows):
     wl = make_workload(name)
     inp = make_inputs(wl)
