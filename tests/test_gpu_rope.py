@@ -72,29 +72,35 @@ def test_rope_small_all_rows(name, base):
     assert max(errs) <= TOL_REL_ROW
 
 
-def _wide_inputs():
-    # a group of rank 470 spans 15 key chunks: wider than the resident-factor
-    # kernel holds at d_h = 128, so the general (per-chunk staging) kernel runs
+def _wide_inputs(head_dim=128):
+    # a group wider than the resident-factor kernel holds (14 key chunks at
+    # d_h = 128, 28 at 64), so the general (per-chunk staging) kernel runs:
+    # rank 470 spans 15 chunks; at d_h 64, rank 900 over 15 heads spans 29
     from test_gpu_parity import _groups
     from workloads.configs import custom_workload
-    lens = (1500, 70, 640)
-    wl = custom_workload(name="wide_group", seed=321, hidden=1024, num_q_heads=16, num_kv_heads=8,
-                         head_dim=128, group_of_kv=_groups((5, 3), 11), group_rank=(470, 96),
-                         value_rank=256, dtype="bf16", batch=len(lens), seq_lens=lens,
-                         prefill_lens=lens, factor_scheme="orthonormal", permute_pages=True)
+    if head_dim == 128:
+        lens, kvh, sizes, ranks = (1500, 70, 640), 8, (5, 3), (470, 96)
+    else:
+        lens, kvh, sizes, ranks = (700, 65), 16, (15, 1), (900, 40)
+    wl = custom_workload(name=f"wide_group_d{head_dim}", seed=321, hidden=1024,
+                         num_q_heads=2 * kvh, num_kv_heads=kvh, head_dim=head_dim,
+                         group_of_kv=_groups(sizes, 11), group_rank=ranks, value_rank=256,
+                         dtype="bf16", batch=len(lens), seq_lens=lens, prefill_lens=lens,
+                         factor_scheme="orthonormal", permute_pages=True)
     return wl, make_inputs(wl)
 
 
-@pytest.mark.parametrize("split", [512, 1024])
-def test_rope_wide_group_general_kernel(split):
-    wl, inp = _wide_inputs()
+@pytest.mark.parametrize("split, head_dim", [(512, 128), (1024, 128), (256, 64)])
+def test_rope_wide_group_general_kernel(split, head_dim):
+    wl, inp = _wide_inputs(head_dim)
     plan = plan_for(wl, split)
-    print(f"[rope] wide_group split {split}", flush=True)
+    print(f"[rope] wide_group d_h {head_dim} split {split}", flush=True)
     pool = gpu_pool_with_append(inp, plan)
     out = _run(inp, plan, pool, 10000.0)
     ref = _rope_rows(inp, [(b, h) for b in range(wl.batch) for h in range(wl.num_q_heads)], 10000.0)
     errs = [row_rel_err(out[b, h], o) for (b, h), o in ref.items()]
-    print(f"[rope] wide_group/{split}: max row rel err {max(errs):.3e} over {len(errs)} rows", flush=True)
+    print(f"[rope] wide_group d_h {head_dim}/{split}: max row rel err {max(errs):.3e} over {len(errs)} rows",
+          flush=True)
     assert max(errs) <= TOL_REL_ROW
 
 
