@@ -69,3 +69,40 @@ def test_graph_replays_equal_eager(Q):
         assert torch.equal(out, eager), f"replay {r} differs"
         assert torch.equal(t["pool"], pool_eager), f"replay {r} pool differs"
         del scratch
+
+
+def test_rotary_graph_replays_equal_eager():
+    # the rotary decode (factor transpose, key rebuild, value pass, merge,
+    # up-projection) records no memset and allocates nothing either
+    from paper_2607_24331_amd import decode_rope, latent_append
+    wl, plan, t, out, _ = _setup(1)
+    max_ctx = max(wl.seq_lens)
+    ws = torch.empty(plan.rope_workspace_bytes(wl.batch, max_ctx), dtype=torch.uint8, device="cuda")
+
+    def step():
+        latent_append(plan, t["x"], t["Lk"], t["Lv"], t["slot"], t["pool"])
+        decode_rope(plan, t["q"], t["pool"], t["table"], t["lens"], max_ctx, t["Rk"], t["Rv"],
+                    rope_base=10000.0, out=out, workspace=ws)
+
+    step()
+    torch.cuda.synchronize()
+    eager = out.clone()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    torch.cuda.synchronize()
+    for r in range(4):
+        out.fill_(float("nan"))
+        ws.fill_(0xAB)                          # stale workspace contents must not matter
+        scratch = torch.randn(1 << 20, device="cuda").sum()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager), f"replay {r} differs"
+        del scratch
