@@ -320,6 +320,21 @@ int dckv_gram(const void* A, int32_t dtype, int64_t rows, int32_t cols, int32_t 
 int dckv_head_similarity(const float* G, int32_t num_heads, int32_t head_dim, float* S,
                          void* stream);
 
+/* Host: the whole merge sequence of Algorithm 1's head clustering
+ * (ClusterHeads, Sec. III-C; the paper names agglomerative clustering):
+ * average linkage on the distance 1 - S[i][j], h - 1 merges from h singleton
+ * clusters down to one.  A cluster is named by its smallest head.  Merge s
+ * joins clusters merge_a[s] < merge_b[s] (the merged cluster keeps the name
+ * merge_a[s]) at linkage distance height[s]; on equal distances the pair
+ * whose names are lexicographically smallest merges first.  Cutting the
+ * sequence after h - K merges gives the K-group clustering of
+ * dckv_cluster_heads, so one call serves every candidate K.
+ *   S host [h][h] double (symmetric); merge_a, merge_b host [h - 1] (out);
+ *   height host [h - 1] (out, may be NULL).
+ * 1 <= h <= DCKV_MAX_HEADS.  Makes no HIP call. */
+int dckv_cluster_merges(const double* S, int32_t num_heads, int32_t* merge_a, int32_t* merge_b,
+                        double* height);
+
 /* Host: Algorithm 1's head clustering (ClusterHeads, Sec. III-C):
  * agglomerative clustering into K groups with average linkage on the
  * distance 1 - S[i][j]; on equal distances the pair of clusters whose
@@ -336,6 +351,8 @@ int dckv_cluster_heads(const double* S, int32_t num_heads, int32_t K, int32_t* g
  *   sum_i r_i alpha_i <= 4 r / h) or sum_i ranks[i] > r, lower by one the
  *   rank with the smallest sigma_i[r_i - 1]^2 * h / heads[i] among ranks
  *   above 1 (equal costs: the lower group id); h = sum of heads.
+ *   Since a group's costs grow as its rank falls, the lowering steps are
+ *   taken in ascending (cost, group id) order across the groups.
  *   heads [K], energy [K] (||W_i||_F^2), rank_cap [K] (min(m, h_i d_h)),
  *   sigma [K][sigma_stride] (singular values of W_i, descending, at least
  *   rank_cap[i] of them) -- all host; init_ranks, ranks [K] host (out).

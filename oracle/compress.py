@@ -10,10 +10,12 @@ one step of the method in the paper's order.
                             centred X, Y (Sec. III-A)
   head_similarity(A, h, d)  S[i][j] = CKA between the activations of head i
                             and head j: columns i*d .. i*d+d-1 of A (Sec. III-C)
+  linkage_distance(D,A,B)   average linkage: mean of D over member pairs
   cluster_heads(S, K)       agglomerative clustering of the heads into K
                             groups (Alg. 1, ClusterHeads)
   energy(W)                 sum of squared singular values = ||W||_F^2
   init_ranks_by_energy      r_i = round(r E_i / E)  (Sec. III-C equation)
+  greedy_cost               Delta E_i / alpha_i of lowering group i's rank
   greedy_adjust             lower the rank with the smallest Delta E_i / alpha_i
                             until the budget holds (Sec. III-C)
   group_decompose           per-group truncated SVD, L = U S^1/2, R = S^1/2 V^T
@@ -77,6 +79,11 @@ def head_similarity(acts: np.ndarray, num_heads: int, head_dim: int) -> np.ndarr
 
 
 # ---------------------------------------------------------------- Sec. III-C
+def linkage_distance(D: np.ndarray, A: Sequence[int], B: Sequence[int]) -> float:
+    """Average linkage: the mean of D over the member pairs of clusters A, B."""
+    return float(np.mean([D[i, j] for i in A for j in B]))
+
+
 def cluster_heads(S: np.ndarray, K: int) -> List[List[int]]:
     """Average-linkage agglomerative clustering on 1 - S down to K groups."""
     h = S.shape[0]
@@ -87,10 +94,7 @@ def cluster_heads(S: np.ndarray, K: int) -> List[List[int]]:
         best = None
         for a in range(len(clusters)):
             for b in range(a + 1, len(clusters)):
-                # mean over member pairs, summed in member order
-                d = sum(float(D[i, j]) for i in clusters[a] for j in clusters[b]) / (
-                    len(clusters[a]) * len(clusters[b]))
-                key = (d, min(clusters[a]), min(clusters[b]))
+                key = (linkage_distance(D, clusters[a], clusters[b]), min(clusters[a]), min(clusters[b]))
                 if best is None or key < best[0]:
                     best = (key, a, b)
         _, a, b = best
@@ -136,6 +140,12 @@ def budget_holds(ranks: Sequence[int], heads: Sequence[int], r: int) -> bool:
     return sum(Fraction(ri * hi, h) for ri, hi in zip(ranks, heads)) <= Fraction(4 * r, h)
 
 
+def greedy_cost(sigma_i: np.ndarray, r_i: int, h_i: int, h: int) -> float:
+    """Delta E_i / alpha_i: the energy of group i's last kept singular value
+    per unit of the budget its removal frees (alpha_i = h_i / h)."""
+    return float(sigma_i[r_i - 1] ** 2 / (h_i / h))
+
+
 def greedy_adjust(ranks: Sequence[int], sigmas: Sequence[np.ndarray], heads: Sequence[int],
                   r: int) -> List[int]:
     """Drop one rank at a time from the group with the smallest
@@ -148,8 +158,7 @@ def greedy_adjust(ranks: Sequence[int], sigmas: Sequence[np.ndarray], heads: Seq
         for i, (ri, hi) in enumerate(zip(ranks, heads)):
             if ri <= 1:
                 continue
-            s = float(sigmas[i][ri - 1])
-            cost = s * s * h / hi                         # Delta E_i / alpha_i, alpha_i = h_i / h
+            cost = greedy_cost(sigmas[i], ri, hi, h)
             if best is None or cost < best[0]:
                 best = (cost, i)
         if best is None:                                  # every group is at rank 1

@@ -95,6 +95,7 @@ SIGNATURES = {
     "dckv_gram_workspace_bytes": (ctypes.c_int, [_i64, _i32, _i32, ctypes.POINTER(ctypes.c_size_t)]),
     "dckv_gram": (ctypes.c_int, [_vp, _i32, _i64, _i32, _i32, _vp, _vp, ctypes.c_size_t, _vp]),
     "dckv_head_similarity": (ctypes.c_int, [_vp, _i32, _i32, _vp, _vp]),
+    "dckv_cluster_merges": (ctypes.c_int, [_vp, _i32, _pi32, _pi32, _vp]),
     "dckv_cluster_heads": (ctypes.c_int, [_vp, _i32, _i32, _pi32]),
     "dckv_allocate_ranks": (ctypes.c_int, [_i32, _pi32, _vp, ctypes.c_double, _vp, _i32, _pi32, _i32,
                                            _pi32, _pi32]),

@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <utility>
 #include <vector>
 
 #include "internal.h"
@@ -57,42 +58,75 @@ int dckv_head_similarity(const float* G, int32_t num_heads, int32_t head_dim, fl
   return DCKV_OK;
 }
 
+int dckv_cluster_merges(const double* S, int32_t num_heads, int32_t* merge_a, int32_t* merge_b,
+                        double* height) {
+  if (!S || (num_heads > 1 && (!merge_a || !merge_b)))
+    return fail(DCKV_EINVAL, "cluster_merges: null S or output");
+  const int h = num_heads;
+  if (h < 1 || h > DCKV_MAX_HEADS)
+    return fail(DCKV_EINVAL, "cluster_merges: num_heads %d outside [1,%d]", h, DCKV_MAX_HEADS);
+  // A cluster is named by its smallest head.  d[a][b] is the average of
+  // 1 - S over the member pairs of clusters a and b; after a and b merge
+  // into a (a < b), the merged cluster's distance to any other cluster c is
+  // the size-weighted mean (n_a d[a][c] + n_b d[b][c]) / (n_a + n_b), which
+  // is that average over the merged member pairs again.
+  double d[DCKV_MAX_HEADS][DCKV_MAX_HEADS];
+  int size[DCKV_MAX_HEADS];
+  bool live[DCKV_MAX_HEADS];
+  for (int i = 0; i < h; ++i) {
+    size[i] = 1;
+    live[i] = true;
+    for (int j = 0; j < h; ++j) d[i][j] = 1.0 - S[i * h + j];
+  }
+  for (int step = 0; step + 1 < h; ++step) {
+    // the closest pair; scanning (a, b) in ascending order of the clusters'
+    // smallest heads makes the first of equal distances the lexicographically
+    // smallest pair
+    int ba = -1, bb = -1;
+    for (int a = 0; a < h; ++a) {
+      if (!live[a]) continue;
+      for (int b = a + 1; b < h; ++b)
+        if (live[b] && (ba < 0 || d[a][b] < d[ba][bb])) {
+          ba = a;
+          bb = b;
+        }
+    }
+    merge_a[step] = ba;
+    merge_b[step] = bb;
+    if (height) height[step] = d[ba][bb];
+    const double wa = size[ba], wb = size[bb], w = wa + wb;
+    for (int c = 0; c < h; ++c) {
+      if (!live[c] || c == ba || c == bb) continue;
+      const double v = (wa * d[ba][c] + wb * d[bb][c]) / w;
+      d[ba][c] = v;
+      d[c][ba] = v;
+    }
+    size[ba] += size[bb];
+    live[bb] = false;
+  }
+  return DCKV_OK;
+}
+
 int dckv_cluster_heads(const double* S, int32_t num_heads, int32_t K, int32_t* group_of_head) {
   if (!S || !group_of_head) return fail(DCKV_EINVAL, "cluster_heads: null S or output");
   const int h = num_heads;
   if (h < 1 || h > DCKV_MAX_HEADS) return fail(DCKV_EINVAL, "cluster_heads: num_heads %d outside [1,%d]", h, DCKV_MAX_HEADS);
   if (K < 1 || K > h) return fail(DCKV_EINVAL, "cluster_heads: K %d outside [1,%d]", K, h);
-  // clusters as sorted member lists; the distance between clusters is the
-  // mean over member pairs of 1 - S[i][j], summed in member order
-  std::vector<std::vector<int>> cl(h);
-  for (int i = 0; i < h; ++i) cl[i] = {i};
-  while (int(cl.size()) > K) {
-    int ba = -1, bb = -1;
-    double bd = 0.0;
-    for (int a = 0; a < int(cl.size()); ++a)
-      for (int b = a + 1; b < int(cl.size()); ++b) {
-        double s = 0.0;
-        for (int i : cl[a])
-          for (int j : cl[b]) s += 1.0 - S[i * h + j];
-        const double d = s / double(cl[a].size() * cl[b].size());
-        // clusters are kept ordered by smallest member, so (a, b) order is the
-        // lexicographic order of (min a, min b)
-        if (ba < 0 || d < bd) {
-          bd = d;
-          ba = a;
-          bb = b;
-        }
-      }
-    std::vector<int> merged = cl[ba];
-    merged.insert(merged.end(), cl[bb].begin(), cl[bb].end());
-    std::sort(merged.begin(), merged.end());
-    cl.erase(cl.begin() + bb);
-    cl.erase(cl.begin() + ba);
-    cl.push_back(merged);
-    std::sort(cl.begin(), cl.end(), [](const std::vector<int>& x, const std::vector<int>& y) { return x[0] < y[0]; });
-  }
-  for (int g = 0; g < int(cl.size()); ++g)
-    for (int i : cl[g]) group_of_head[i] = g;
+  int32_t ma[DCKV_MAX_HEADS], mb[DCKV_MAX_HEADS];
+  const int st = dckv_cluster_merges(S, h, ma, mb, nullptr);
+  if (st != DCKV_OK) return st;
+  // the first h - K merges of the sequence leave K clusters; each head
+  // follows its cluster's name (smallest head) through the merges
+  int root[DCKV_MAX_HEADS];
+  for (int i = 0; i < h; ++i) root[i] = i;
+  for (int s = 0; s < h - K; ++s)
+    for (int i = 0; i < h; ++i)
+      if (root[i] == mb[s]) root[i] = ma[s];
+  // groups numbered in ascending order of their smallest head
+  int label[DCKV_MAX_HEADS];
+  int next = 0;
+  for (int i = 0; i < h; ++i) label[i] = (root[i] == i) ? next++ : -1;
+  for (int i = 0; i < h; ++i) group_of_head[i] = label[root[i]];
   return DCKV_OK;
 }
 
@@ -111,33 +145,40 @@ int dckv_allocate_ranks(int32_t K, const int32_t* heads, const double* energy,
       return fail(DCKV_EINVAL, "allocate_ranks: rank cap %d of group %d outside [1, sigma_stride %d]", rank_cap[i], i, sigma_stride);
     h += heads[i];
   }
+  int64_t weighted = 0, total = 0;          // sum r_i h_i and sum r_i
   for (int i = 0; i < K; ++i) {
     const int ri = int(std::floor(double(r) * energy[i] / energy_total + 0.5));
     init_ranks[i] = std::max(1, std::min(ri, rank_cap[i]));
     ranks[i] = init_ranks[i];
+    weighted += int64_t(ranks[i]) * heads[i];
+    total += ranks[i];
   }
-  auto holds = [&]() {
-    int64_t weighted = 0, total = 0;
-    for (int i = 0; i < K; ++i) {
-      weighted += int64_t(ranks[i]) * heads[i];
-      total += ranks[i];
-    }
-    return weighted <= 4 * int64_t(r) && total <= r;
+  // Lowering group i from rank k to k - 1 costs sigma_{i,k}^2 * h / h_i, and
+  // a group's costs only grow as its rank falls (singular values descend).
+  // So the greedy rule -- always the cheapest single step, the lower group
+  // id on equal costs -- takes the steps of all groups in ascending
+  // (cost, group) order: a min-heap holding each group's next step.
+  auto cost = [&](int i) {
+    const double s = sigma[int64_t(i) * sigma_stride + ranks[i] - 1];
+    return s * s * double(h) / double(heads[i]);
   };
-  while (!holds()) {
-    int best = -1;
-    double bc = 0.0;
-    for (int i = 0; i < K; ++i) {
-      if (ranks[i] <= 1) continue;
-      const double s = sigma[int64_t(i) * sigma_stride + ranks[i] - 1];
-      const double c = s * s * double(h) / double(heads[i]);
-      if (best < 0 || c < bc) {
-        bc = c;
-        best = i;
-      }
+  std::vector<std::pair<double, int>> heap;
+  heap.reserve(K);
+  auto later = [](const std::pair<double, int>& x, const std::pair<double, int>& y) { return x > y; };
+  for (int i = 0; i < K; ++i)
+    if (ranks[i] > 1) heap.emplace_back(cost(i), i);
+  std::make_heap(heap.begin(), heap.end(), later);
+  while ((weighted > 4 * int64_t(r) || total > r) && !heap.empty()) {
+    std::pop_heap(heap.begin(), heap.end(), later);
+    const int i = heap.back().second;
+    heap.pop_back();
+    --ranks[i];
+    weighted -= heads[i];
+    --total;
+    if (ranks[i] > 1) {
+      heap.emplace_back(cost(i), i);
+      std::push_heap(heap.begin(), heap.end(), later);
     }
-    if (best < 0) break;                         // every group at rank 1
-    --ranks[best];
   }
   return DCKV_OK;
 }

@@ -354,6 +354,23 @@ def cluster_heads(S, K: int):
     return list(out)
 
 
+def cluster_merges(S):
+    """The clustering's whole merge sequence (host call): a list of
+    (a, b, height) -- clusters named by their smallest head, a < b, merged at
+    average-linkage distance `height` -- h - 1 entries in merge order."""
+    import numpy as np
+    Sd = np.ascontiguousarray(np.asarray(S, dtype=np.float64))
+    h = Sd.shape[0]
+    if Sd.shape != (h, h):
+        raise ValueError("S must be square")
+    n = max(h - 1, 1)
+    ma, mb = (ctypes.c_int32 * n)(), (ctypes.c_int32 * n)()
+    ht = (ctypes.c_double * n)()
+    _check(_lib.dckv_cluster_merges(Sd.ctypes.data_as(ctypes.c_void_p), h, ma, mb,
+                                    ctypes.cast(ht, ctypes.c_void_p)), "cluster_merges")
+    return [(ma[i], mb[i], ht[i]) for i in range(h - 1)]
+
+
 def allocate_ranks(heads: Sequence[int], energy: Sequence[float], energy_total: float,
                    sigmas: Sequence, rank_cap: Sequence[int], r: int):
     """(init_ranks, ranks) of the energy rule and the greedy budget step (host call)."""

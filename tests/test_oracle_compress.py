@@ -133,6 +133,32 @@ def test_greedy_adjust_hand_worked():
     assert out2 == [2, 6]
 
 
+def test_greedy_adjust_paper_budget_alone():
+    # A case where only the paper's inequality binds (sum r_i = 8 = r from the
+    # start, so the extra sum r_i <= r condition never acts): heads (2, 6),
+    # h = 8, r = 8, so sum r_i h_i <= 4 r = 32 is required; start [2, 6] gives 40.
+    # Costs sigma^2 / alpha: group 0 at rank 2: 2^2 * 8/2 = 16; group 1 at rank
+    # 6: 2^2 * 8/6 = 5.33, then at rank 5: 2.5^2 * 8/6 = 8.33 -- group 1 twice,
+    # ending at [2, 4] (4 + 24 = 28 <= 32).  An unnormalised rule ties 4 = 4 at
+    # the first step, lowers group 0 and ends at [1, 5].
+    sig0 = np.array([3.0, 2.0])
+    sig1 = np.array([6.0, 5.0, 4.0, 3.0, 2.5, 2.0])
+    assert not oc.budget_holds([2, 6], [2, 6], 8)
+    assert oc.greedy_adjust([2, 6], [sig0, sig1], [2, 6], 8) == [2, 4]
+    assert oc.greedy_cost(sig0, 2, 2, 8) == pytest.approx(16.0)
+    assert oc.greedy_cost(sig1, 6, 6, 8) == pytest.approx(16.0 / 3.0)
+
+
+def test_linkage_distance_is_the_pair_mean():
+    D = np.array([[0.0, 0.2, 0.4, 0.9],
+                  [0.2, 0.0, 0.6, 0.5],
+                  [0.4, 0.6, 0.0, 0.3],
+                  [0.9, 0.5, 0.3, 0.0]])
+    assert oc.linkage_distance(D, [0, 1], [2]) == pytest.approx(0.5)
+    assert oc.linkage_distance(D, [0, 1], [2, 3]) == pytest.approx((0.4 + 0.9 + 0.6 + 0.5) / 4)
+    assert oc.linkage_distance(D, [3], [0]) == pytest.approx(0.9)
+
+
 def test_group_decompose_eckart_young_and_balance():
     g = np.random.default_rng(6)
     Wi = g.standard_normal((20, 12))
