@@ -243,10 +243,13 @@ __global__ __launch_bounds__(WR * WC * 64) void gram_tiles(const T* __restrict__
 }
 
 // F[i][j] = ||G_ij||_F^2, one work-group a block, fixed-order sums; F is
-// written into S's memory and turned into S by head_sim_finish.
+// written into S's memory and turned into S by head_sim_finish.  Both
+// (i, j) and (j, i) sum the block above the diagonal in the same order, so
+// F, and with it S, is exactly symmetric as linear CKA is.
 __global__ __launch_bounds__(256) void head_sim_blocks(const float* __restrict__ G, int h, int d,
                                                        float* __restrict__ F) {
-  const int i = blockIdx.x, j = blockIdx.y;
+  const int bx = blockIdx.x, by = blockIdx.y;
+  const int i = min(bx, by), j = max(bx, by);
   const int n = h * d, tid = threadIdx.x;
   __shared__ float red[256];
   float f = 0.f;
@@ -260,7 +263,7 @@ __global__ __launch_bounds__(256) void head_sim_blocks(const float* __restrict__
     if (tid < s) red[tid] += red[tid + s];
     __syncthreads();
   }
-  if (tid == 0) F[i * h + j] = red[0];
+  if (tid == 0) F[bx * h + by] = red[0];
 }
 
 // S[i][j] = F[i][j] / (sqrt(F[i][i]) sqrt(F[j][j])) in place: one work-group

@@ -85,7 +85,9 @@ def test_head_similarity_matches_oracle():
         S = key_similarity(torch.from_numpy(acts).cuda(), h, d)
         torch.cuda.synchronize()
         ref = oc.head_similarity(acts.astype(np.float64), h, d)
-        assert np.max(np.abs(S.double().cpu().numpy() - ref)) <= 1e-4
+        Sh = S.double().cpu().numpy()
+        assert np.max(np.abs(Sh - ref)) <= 1e-4
+        assert np.array_equal(Sh, Sh.T)                     # CKA is symmetric: exactly so here
 
 
 def test_head_similarity_full_size_sampled():
