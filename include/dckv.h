@@ -216,6 +216,25 @@ int dckv_decode(const dckv_plan* plan, const float* q, int32_t batch, const void
                 const void* R_value, float* out, void* workspace, size_t workspace_bytes,
                 void* stream);
 
+/* Decode that allocates nothing, for callers that cannot allocate device
+ * memory or pass a workspace: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  Same computation, kernels,
+ * arguments, validation and bitwise results as dckv_decode, without the
+ * workspace: the scratch lives in a fixed device array of
+ * DCKV_NOALLOC_SCRATCH_BYTES that each GPU the library runs on holds until
+ * the process ends.  A call whose dckv_decode_workspace_bytes exceeds that
+ * size returns DCKV_EWORKSPACE and enqueues nothing.  The call itself never
+ * calls hipMalloc or hipFree; the first call on a device looks the array's
+ * address up once (hipGetSymbolAddress).  Every call on one GPU shares that
+ * GPU's array: calls that may overlap on one GPU (different streams, several
+ * threads) race and must be ordered by the caller.  The array needs no
+ * clearing: every byte a call reads was written earlier in that call. */
+#define DCKV_NOALLOC_SCRATCH_BYTES (64u << 20)
+int dckv_decode_noalloc(const dckv_plan* plan, const float* q, int32_t batch, const void* pool,
+                        int64_t num_pages, const int32_t* page_table, int32_t max_pages,
+                        const int32_t* seq_lens, int32_t max_context, const void* R_keys,
+                        const void* R_value, float* out, void* stream);
+
 /* Benchmark instrumentation (not part of the method).  With two non-NULL
  * hipEvent_t handles, every later dckv_decode on this plan launches its
  * split-K attention kernel (the dominant kernel of a decode; for

@@ -24,6 +24,7 @@ DCKV_ENOMEM = -6
 DCKV_F32 = 0
 DCKV_BF16 = 1
 PAGE_TOKENS = 64
+NOALLOC_SCRATCH_BYTES = 64 << 20
 
 STATUS_NAMES = {0: "DCKV_OK", -1: "DCKV_EINVAL", -2: "DCKV_EDTYPE", -3: "DCKV_EALIGN",
                 -4: "DCKV_EWORKSPACE", -5: "DCKV_EHIP", -6: "DCKV_ENOMEM"}
@@ -83,6 +84,8 @@ SIGNATURES = {
     "dckv_latent_append": (ctypes.c_int, [_vp, _vp, _i32, _vp, _vp, _vp, _vp, _i64, _vp]),
     "dckv_decode": (ctypes.c_int, [_vp, _vp, _i32, _vp, _i64, _vp, _i32, _vp, _i32, _vp, _vp, _vp,
                                    _vp, ctypes.c_size_t, _vp]),
+    "dckv_decode_noalloc": (ctypes.c_int, [_vp, _vp, _i32, _vp, _i64, _vp, _i32, _vp, _i32, _vp,
+                                           _vp, _vp, _vp]),
     "dckv_plan_set_profile_events": (ctypes.c_int, [_vp, _vp, _vp]),
     "dckv_rope_workspace_bytes": (ctypes.c_int, [_vp, _i32, _i32, ctypes.POINTER(ctypes.c_size_t)]),
     "dckv_decode_rope": (ctypes.c_int, [_vp, _vp, _i32, _vp, _i64, _vp, _i32, _vp, _i32, _vp, _vp,

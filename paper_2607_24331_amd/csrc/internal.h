@@ -133,6 +133,12 @@ hipError_t launch_gram(const void* A, int32_t dtype, int64_t rows, int32_t cols,
 hipError_t launch_head_similarity(const float* G, int32_t h, int32_t d, float* S,
                                   hipStream_t stream);
 
+// Host checks of a decode call (all but the workspace) and its launch shape.
+int check_decode(const char* where, const dckv_plan* p, const float* q, int32_t batch,
+                 const void* pool, int64_t num_pages, const int32_t* page_table, int32_t max_pages,
+                 const int32_t* seq_lens, int32_t max_context, const void* R_keys,
+                 const void* R_value, const float* out, DecodeShape* shape);
+
 // Builds plan.mfma and sets plan.mfma_ok (host only, no HIP call).
 void build_mfma_tables(dckv_plan& p);
 

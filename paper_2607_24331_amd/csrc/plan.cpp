@@ -214,6 +214,32 @@ void build_rope_tables(dckv_plan& p) {
     }
 }
 
+// Host checks shared by the decode entry points: every argument except the
+// workspace, then the launch shape.  Returns DCKV_OK with *shape set (for
+// batch == 0 nothing else is checked), or a failure status.
+int check_decode(const char* where, const dckv_plan* p, const float* q, int32_t batch,
+                 const void* pool, int64_t num_pages, const int32_t* page_table, int32_t max_pages,
+                 const int32_t* seq_lens, int32_t max_context, const void* R_keys,
+                 const void* R_value, const float* out, DecodeShape* shape) {
+  if (!p) return fail(DCKV_EINVAL, "%s: null plan", where);
+  if (batch < 0) return fail(DCKV_EINVAL, "%s: batch %d < 0", where, batch);
+  if (batch == 0) return DCKV_OK;
+  if (!q || !pool || !page_table || !seq_lens || !R_keys || !R_value || !out)
+    return fail(DCKV_EINVAL, "%s: null device pointer", where);
+  if (int64_t(batch) * p->Q > 65535)
+    return fail(DCKV_EINVAL, "%s: batch %d x queries %d above 65535", where, batch, p->Q);
+  if (num_pages < 1) return fail(DCKV_EINVAL, "%s: num_pages %lld < 1", where, (long long)num_pages);
+  if (max_pages < 1) return fail(DCKV_EINVAL, "%s: max_pages %d < 1", where, max_pages);
+  if (max_context < 0 || int64_t(max_context) > int64_t(max_pages) * DCKV_PAGE_TOKENS)
+    return fail(DCKV_EINVAL, "%s: max_context %d outside [0, max_pages*64 = %lld]", where,
+                max_context, (long long)max_pages * DCKV_PAGE_TOKENS);
+  if (!aligned(q, 16) || !aligned(pool, 16) || !aligned(R_keys, 16) || !aligned(R_value, 16) ||
+      !aligned(out, 16) || !aligned(page_table, 4) || !aligned(seq_lens, 4))
+    return fail(DCKV_EALIGN, "%s: q, pool, R_keys, R_value and out must be 16-byte aligned", where);
+  *shape = decode_shape(*p, batch, max_context);
+  return DCKV_OK;
+}
+
 }  // namespace dckv
 
 extern "C" {
@@ -418,23 +444,12 @@ int dckv_decode(const dckv_plan* p, const float* q, int32_t batch, const void* p
                 const int32_t* seq_lens, int32_t max_context, const void* R_keys,
                 const void* R_value, float* out, void* workspace, size_t workspace_bytes,
                 void* stream) {
-  if (!p) return fail(DCKV_EINVAL, "decode: null plan");
-  if (batch < 0) return fail(DCKV_EINVAL, "decode: batch %d < 0", batch);
-  if (batch == 0) return DCKV_OK;
-  if (!q || !pool || !page_table || !seq_lens || !R_keys || !R_value || !out || !workspace)
-    return fail(DCKV_EINVAL, "decode: null device pointer");
-  if (int64_t(batch) * p->Q > 65535)
-    return fail(DCKV_EINVAL, "decode: batch %d x queries %d above 65535", batch, p->Q);
-  if (num_pages < 1) return fail(DCKV_EINVAL, "decode: num_pages %lld < 1", (long long)num_pages);
-  if (max_pages < 1) return fail(DCKV_EINVAL, "decode: max_pages %d < 1", max_pages);
-  if (max_context < 0 || int64_t(max_context) > int64_t(max_pages) * DCKV_PAGE_TOKENS)
-    return fail(DCKV_EINVAL, "decode: max_context %d outside [0, max_pages*64 = %lld]", max_context,
-                (long long)max_pages * DCKV_PAGE_TOKENS);
-  if (!aligned(q, 16) || !aligned(pool, 16) || !aligned(R_keys, 16) || !aligned(R_value, 16) ||
-      !aligned(out, 16) || !aligned(page_table, 4) || !aligned(seq_lens, 4))
-    return fail(DCKV_EALIGN, "decode: q, pool, R_keys, R_value and out must be 16-byte aligned");
+  dckv::DecodeShape shape;
+  int st = dckv::check_decode("decode", p, q, batch, pool, num_pages, page_table, max_pages,
+                              seq_lens, max_context, R_keys, R_value, out, &shape);
+  if (st != DCKV_OK || batch == 0) return st;
+  if (!workspace) return fail(DCKV_EINVAL, "decode: null device pointer");
   if (!aligned(workspace, 256)) return fail(DCKV_EALIGN, "decode: workspace must be 256-byte aligned");
-  const dckv::DecodeShape shape = dckv::decode_shape(*p, batch, max_context);
   if (workspace_bytes < shape.bytes)
     return fail(DCKV_EWORKSPACE, "decode: workspace of %zu bytes, %zu needed", workspace_bytes,
                 shape.bytes);

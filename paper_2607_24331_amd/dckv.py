@@ -209,6 +209,38 @@ def decode(plan: Plan, q: torch.Tensor, pool: torch.Tensor, page_table: torch.Te
     return out
 
 
+def decode_noalloc(plan: Plan, q: torch.Tensor, pool: torch.Tensor, page_table: torch.Tensor,
+                   seq_lens: torch.Tensor, max_context: int, R_keys: torch.Tensor,
+                   R_value: torch.Tensor, out: torch.Tensor, stream=None) -> torch.Tensor:
+    """decode() without a workspace: the library's fixed device scratch array
+    serves instead (dckv_decode_noalloc).  `out` must be given, so that the
+    call allocates nothing; calls that overlap on one GPU race."""
+    Q = plan.queries_per_seq
+    if q.dim() == 3 and Q == 1:
+        qshape = (q.shape[0], plan.num_q_heads, plan.head_dim)
+    elif q.dim() == 4:
+        qshape = (q.shape[0], Q, plan.num_q_heads, plan.head_dim)
+    else:
+        raise ValueError("q must be [batch, Q, H_q, d_h] (or [batch, H_q, d_h] with Q = 1)")
+    B = q.shape[0]
+    dt = plan.torch_dtype
+    pq = _dev(q, "q", torch.float32, qshape)
+    pp = _dev(pool, "pool", dt)
+    if page_table.dim() != 2 or page_table.shape[0] != B:
+        raise ValueError("page_table must be [batch, max_pages]")
+    pt = _dev(page_table, "page_table", torch.int32)
+    psl = _dev(seq_lens, "seq_lens", torch.int32, (B,))
+    prk = _dev(R_keys, "R_keys", dt)
+    if R_keys.numel() != plan.key_factor_elems:
+        raise ValueError(f"R_keys holds {R_keys.numel()} elements, expected {plan.key_factor_elems}")
+    prv = _dev(R_value, "R_value", dt, (plan.value_rank, plan.num_kv_heads * plan.head_dim))
+    po = _dev(out, "out", torch.float32, qshape)
+    _check(_lib.dckv_decode_noalloc(plan.handle, pq, B, pp, _num_pages(plan, pool), pt,
+                                    page_table.shape[1], psl, int(max_context), prk, prv, po,
+                                    _stream_handle(stream)), "decode_noalloc")
+    return out
+
+
 def decode_rope(plan: Plan, q: torch.Tensor, pool: torch.Tensor, page_table: torch.Tensor,
                 seq_lens: torch.Tensor, max_context: int, R_keys: torch.Tensor,
                 R_value: torch.Tensor, rope_base: float = 10000.0,

@@ -151,6 +151,32 @@ def test_call_validation_never_launches(lib):
     assert call(batch=0) == capi.DCKV_OK                      # no-op
 
 
+@pytest.mark.skipif(torch.cuda.is_available(), reason="raw fake pointers are only passed on a host without a GPU")
+def test_noalloc_validation_never_launches(lib):
+    # the decode without a workspace: the same argument checks, then the
+    # scratch bound (64-token splits over 131072 tokens need far more than
+    # the fixed array), all before any HIP call
+    from paper_2607_24331_amd import Plan
+    wl = make_workload("gqa8b_b4_t32k")
+    p = Plan(wl.hidden, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_of_kv, wl.group_rank,
+             wl.value_rank, wl.dtype, 64)
+    A = 1 << 20
+    args = [p.handle, A, 1, A, 4096, A, 2048, A, 131072, A, A, A, None]
+    assert p.workspace_bytes(1, 131072) > capi.NOALLOC_SCRATCH_BYTES
+    assert lib.dckv_decode_noalloc(*args) == capi.DCKV_EWORKSPACE
+    assert "scratch" in lib.dckv_last_error().decode()
+    bad = list(args)
+    bad[1] = None
+    assert lib.dckv_decode_noalloc(*bad) == capi.DCKV_EINVAL
+    bad = list(args)
+    bad[11] = A + 4
+    assert lib.dckv_decode_noalloc(*bad) == capi.DCKV_EALIGN
+    bad = list(args)
+    bad[2] = 0
+    assert lib.dckv_decode_noalloc(*bad) == capi.DCKV_OK      # batch 0: no-op
+    assert lib.dckv_decode_noalloc(None, *args[1:]) == capi.DCKV_EINVAL
+
+
 def test_binding_rejects_host_tensors():
     from paper_2607_24331_amd import decode, latent_append
     wl = make_workload("tiny_mha_f32")
