@@ -40,6 +40,9 @@ def parse():
     ap.add_argument("--split-tokens", type=int, default=0)
     ap.add_argument("--head-slices", type=int, default=0)
     ap.add_argument("--decode-waves", type=int, default=0)
+    ap.add_argument("--decode-passes", type=int, default=0, choices=[0, 1, 2],
+                    help="decode kernels: 0 chosen per call, 1 single-pass split kernel, "
+                         "2 two-pass score and value kernels")
     ap.add_argument("--queries", type=int, default=1,
                     help="causal queries a sequence in each decode (speculative verification / "
                          "chunked prefill); 1 is plain decode")
@@ -445,7 +448,7 @@ def main():
         return main_dense(args, torch, wl)
     plan = Plan(wl.hidden, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_of_kv,
                 wl.group_rank, wl.value_rank, wl.dtype, args.split_tokens, args.head_slices,
-                args.decode_waves, args.queries)
+                args.decode_waves, args.queries, args.decode_passes)
     mfma = bool(plan.geometry["mfma_path"])
     Q = args.queries
     inp = device_inputs(wl, plan, torch, Q)

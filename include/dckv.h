@@ -111,6 +111,15 @@ typedef struct dckv_layer_desc {
                                       or 0 for the default (eight when every wave
                                       gets at least one 16-rank value tile, i.e.
                                       r_v > 112, else four) */
+  int32_t decode_passes;           /* bf16 decode kernels: 0 chooses per call (the
+                                      single-pass split kernel, except for one query a
+                                      sequence and at most 32 query heads when it would
+                                      need several row slices -- value ranks above what
+                                      one slice's accumulators hold -- and the call holds
+                                      at least 2048 page slots, or when it does not
+                                      apply: then the two-pass kernels); 1 never the
+                                      two-pass kernels; 2 always the two-pass kernels
+                                      (DCKV_EINVAL if the layer does not fit them) */
 } dckv_layer_desc;
 
 /* Derived layout facts of a plan. */
@@ -136,6 +145,11 @@ typedef struct dckv_plan_geometry {
                                       summed over its 16-row tiles: a tile loads the chunks of
                                       its rows' groups, so a group cut by a tile boundary is
                                       loaded twice (0 otherwise) */
+  int32_t two_pass;                /* 1 if one-query decodes of this plan may take the
+                                      two-pass MFMA kernels (a score pass writing each
+                                      page's softmax weights, then a value pass over
+                                      value-rank groups), as decode_passes chooses */
+  int32_t reserved0;
   int64_t page_elems;              /* elements per page: 64*R_Kp + 64*r_vp */
   int64_t value_base;              /* element offset of the value part in a page: 64*R_Kp */
   int64_t key_factor_elems;        /* elements of the concatenated R_g blocks */

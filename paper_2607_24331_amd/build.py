@@ -24,7 +24,7 @@ ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 ARCH = "gfx950"
 
 HOST_SOURCES = ["plan.cpp", "offline.cpp"]
-HIP_SOURCES = ["append.hip", "decode.hip", "decode_mfma.hip", "dense.hip", "gram.hip", "rope.hip", "noalloc.hip"]
+HIP_SOURCES = ["append.hip", "decode.hip", "decode_mfma.hip", "dense.hip", "gram.hip", "rope.hip", "noalloc.hip", "decode_pass.hip"]
 
 HIPCC_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

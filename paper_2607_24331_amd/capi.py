@@ -45,6 +45,7 @@ class LayerDesc(ctypes.Structure):
         ("head_slices", ctypes.c_int32),
         ("queries_per_seq", ctypes.c_int32),
         ("decode_waves", ctypes.c_int32),
+        ("decode_passes", ctypes.c_int32),
     ]
 
 
@@ -64,6 +65,8 @@ class PlanGeometry(ctypes.Structure):
         ("decode_ring", ctypes.c_int32),
         ("value_tiles_per_wave", ctypes.c_int32),
         ("key_chunk_loads", ctypes.c_int32),
+        ("two_pass", ctypes.c_int32),
+        ("reserved0", ctypes.c_int32),
         ("page_elems", ctypes.c_int64),
         ("value_base", ctypes.c_int64),
         ("key_factor_elems", ctypes.c_int64),

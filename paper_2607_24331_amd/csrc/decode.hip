@@ -214,7 +214,76 @@ hipError_t launch_decode_t(const dckv_plan& p, const DecodeShape& sh, const floa
 
 }  // namespace
 
+// Two-pass shape.  Score work-groups of eight pages, so that ragged batches
+// balance over the compute units.  Value work-groups (sequence, chunk, rank
+// group): the tiles a group (4, 6 or 8) and the chunk count are chosen so
+// that the work-groups fill whole rounds of the compute units -- the
+// estimate is rounds x (pages a wave x (tiles + head tiles, the weight
+// loads counted at half a tile each) + a fixed cost of 4) -- with fewer
+// chunks (fewer partials) on ties; split_tokens / 64, when given, is the
+// chunk length.
+static DecodeShape pass_shape(const dckv_plan& p, int32_t batch, int32_t max_context) {
+  DecodeShape s{};
+  s.batch = batch;
+  s.max_context = max_context;
+  s.pass = true;
+  const int64_t npm = std::max<int64_t>(1, (int64_t(max_context) + DCKV_PAGE_TOKENS - 1) / DCKV_PAGE_TOKENS);
+  s.npm = int32_t(npm);
+  s.unit_pages = 8;
+  s.units_per_seq = int32_t((npm + s.unit_pages - 1) / s.unit_pages);
+  const int64_t cap = pass_max_chunk_pages();
+  const int64_t B = std::max<int32_t>(batch, 1);
+  int64_t best_cost = -1;
+  for (int32_t rgt : {8, 6, 4}) {
+    const int64_t nrg = (p.pass.mt_v + rgt - 1) / rgt;
+    auto consider = [&](int64_t cp) {
+      const int64_t nc = (npm + cp - 1) / cp;
+      const int64_t rounds = (B * nc * nrg + kTargetWorkgroups - 1) / kTargetWorkgroups;
+      const int64_t cost = rounds * ((cp + 7) / 8 * (rgt + p.pass.nt) + 4);
+      if (best_cost < 0 || cost < best_cost || (cost == best_cost && nc < s.n_chunks)) {
+        best_cost = cost;
+        s.rgt = rgt;
+        s.n_rgroups = int32_t(nrg);
+        s.chunk_pages = int32_t(cp);
+        s.n_chunks = int32_t(nc);
+      }
+    };
+    if (p.split_tokens > 0) {
+      consider(std::min<int64_t>(cap, std::max<int64_t>(1, p.split_tokens / DCKV_PAGE_TOKENS)));
+    } else {
+      for (int64_t nc = (npm + cap - 1) / cap; nc <= std::max<int64_t>(1, 2 * kTargetWorkgroups / (B * nrg)) + 1
+                                               && nc <= npm; ++nc)
+        consider((npm + nc - 1) / nc);
+    }
+  }
+  s.split_tokens = s.chunk_pages * DCKV_PAGE_TOKENS;
+  s.n_split = s.n_chunks;
+  const size_t nh = 16 * size_t(p.pass.nt);
+  s.off_qt = 0;
+  s.off_p = align_up(size_t(batch) * p.pass.max_pairs * 2048, 256);
+  s.off_el = s.off_p + align_up(size_t(batch) * npm * nh * 64 * 2, 256);
+  s.off_ml = s.off_el + align_up(size_t(batch) * npm * p.pass.nt * 512, 256);
+  const size_t rows = size_t(batch) * s.n_chunks;
+  s.off_acc = s.off_ml + align_up(rows * 2 * nh * sizeof(float), 256);
+  s.off_opart = s.off_acc + align_up(rows * nh * size_t(p.rv) * sizeof(float), 256);
+  s.bytes = s.off_opart + align_up(size_t(batch) * p.Hq * p.rv * sizeof(float), 256);
+  return s;
+}
+
 DecodeShape decode_shape(const dckv_plan& p, int32_t batch, int32_t max_context) {
+  // The two-pass kernels when asked for, when the single-pass kernel does not
+  // apply, or when it would cut the rows into several slices (a value rank
+  // beyond what one slice's accumulators hold), each slice reading the whole
+  // value part again, and the batch holds enough pages to give every wave of
+  // the chip one.  Otherwise the single-pass kernel: measured on the one-query
+  // layers it is as fast or faster, the two passes each paying a work-group
+  // prologue and a tail.
+  if (p.pass_ok) {
+    const int64_t npm = (int64_t(max_context) + DCKV_PAGE_TOKENS - 1) / DCKV_PAGE_TOKENS;
+    const bool many_pages = int64_t(batch) * npm >= int64_t(8) * kTargetWorkgroups;
+    if (p.decode_passes == 2 || !p.mfma_ok || (many_pages && p.mfma.n_slices > 1))
+      return pass_shape(p, batch, max_context);
+  }
   DecodeShape s{};
   s.batch = batch;
   s.max_context = max_context;
@@ -222,15 +291,17 @@ DecodeShape decode_shape(const dckv_plan& p, int32_t batch, int32_t max_context)
   int64_t L = p.split_tokens;
   if (L == 0) {
     if (s.mfma) {
-      // about one work-group per compute unit over the whole batch
+      // about one work-group per compute unit over the whole batch, at most
+      // the split kernel's page-list capacity
       const int64_t tokens = int64_t(batch) * max_context * p.mfma.n_slices;
       L = (tokens + kTargetWorkgroups - 1) / kTargetWorkgroups;
       L = std::max<int64_t>(DCKV_PAGE_TOKENS, (L + DCKV_PAGE_TOKENS - 1) / DCKV_PAGE_TOKENS * DCKV_PAGE_TOKENS);
+      L = std::min<int64_t>(L, mfma_max_split_tokens());
     } else {
       L = kValuSplitTokens;
     }
   }
-  if (s.mfma && L > mfma_max_split_tokens()) s.mfma = false;
+  if (s.mfma && L > mfma_max_split_tokens()) s.mfma = false;   // an explicit split beyond the cap
   s.split_tokens = int32_t(L);
   s.n_split = max_context > 0 ? int32_t((max_context + L - 1) / L) : 1;
   s.off_qt = 0;
@@ -259,6 +330,9 @@ hipError_t launch_decode(const dckv_plan& p, const DecodeShape& shape, const flo
                          const void* pool, int64_t num_pages, const int32_t* page_table,
                          int32_t max_pages, const int32_t* seq_lens, const void* R_keys,
                          const void* R_value, float* out, void* workspace, hipStream_t stream) {
+  if (shape.pass)
+    return launch_decode_pass(p, shape, q, pool, num_pages, page_table, max_pages, seq_lens, R_keys,
+                              R_value, out, workspace, stream);
   if (shape.mfma)
     return launch_decode_mfma(p, shape, q, pool, num_pages, page_table, max_pages, seq_lens, R_keys,
                               R_value, out, workspace, stream);

@@ -20,7 +20,7 @@
 //
 // merge_mfma: fixed ascending-split log-sum-exp merge of the partials into
 // the normalised value-latent output a_h (fp32).
-// upproj: o_h = a_h R_v[:, kv(h) block] (Sec. III-A z R, Sec. III-D R_v).
+// The up-projection o_h = a_h R_v[:, kv(h) block] is upproj_rows (decode_pass.hip).
 #include <cmath>
 
 #include "device.h"
@@ -33,7 +33,6 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kRing = 16;                 // loads in flight per wave
 constexpr int kPageSlots = 256;           // pages per split the LDS page list holds
 constexpr int kPStride = 72;              // bf16 per head row of the p tile (64 + pad)
 constexpr int kMergeRanks = 8;            // value ranks per merge work-group
@@ -736,111 +735,6 @@ __global__ __launch_bounds__(256) void merge_mfma(const float* __restrict__ part
   }
 }
 
-// Up-projection o[b][h][:] = a[b][h][:] R_v[:, kv(h) block] (Sec. III-A z R,
-// Sec. III-D R_v).  Grid (row blocks of 8, KV heads, column tiles of 32): a
-// work-group serves every query row (sequence, query, head) of its KV head in its row
-// block, for 32 output columns.  Thread t: 8 columns (one 16-byte load a
-// rank), rank group t/4 (ranks t/4, t/4 + 64, ...), four loads in flight; the
-// 64 rank groups are then summed in a fixed order, one query row a round.
-__global__ __launch_bounds__(256) void upproj(const float* __restrict__ amerged,
-                                              const bf16* __restrict__ Rv,
-                                              float* __restrict__ out, int batch, int rv,
-                                              HeadTables tb) {
-  constexpr int RB = 8;                        // query rows a work-group
-  constexpr int U = 8;                         // R_v loads a batch (two batches in flight)
-  const int rbk = blockIdx.x, kv = blockIdx.y, ct = blockIdx.z;   // row blocks on x: grid x is wide
-  const int tid = threadIdx.x;
-  const int dh = tb.head_dim, n = tb.n_kv_heads * dh, qpk = tb.q_per_kv;
-  const int rows = batch * qpk;
-  const int row0 = rbk * RB;
-  const int nrow = min(RB, rows - row0);
-  if (nrow <= 0) return;
-  extern __shared__ float sa[];                // [RB][rv], then [64][RB][32] partial sums
-  const int c8 = tid % 4, rg = tid / 4;
-  const int col = ct * 32 + 8 * c8;            // first of eight output columns
-  // d_h is a multiple of 8 on this path; threads past d_h load a valid column
-  // group and discard their sums
-  const bf16* src = Rv + int64_t(kv) * dh + min(col, dh - 8);
-  u32x4 v[U];
-  auto issue = [&](int rbase) {
-#pragma unroll
-    for (int k = 0; k < U; ++k) v[k] = load16(src + int64_t(min(rbase + 64 * k, rv - 1)) * n);
-  };
-  issue(rg);                                   // first R_v batch overlaps the staging below
-
-  // stage the merged rows, eight loads in flight a thread
-  const int total = nrow * rv;
-  for (int base = 0; base < total; base += 256 * 8) {
-    float t[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int i = base + tid + 256 * k;
-      t[k] = 0.f;
-      if (i < total) {
-        const int q = i / rv, r = i - q * rv;
-        const int row = row0 + q;
-        const int b = row / qpk, h = kv * qpk + row % qpk;
-        t[k] = amerged[(int64_t(b) * tb.n_q_heads + h) * rv + r];
-      }
-    }
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int i = base + tid + 256 * k;
-      if (i < total) sa[i] = t[k];
-    }
-  }
-  __syncthreads();
-  float acc[RB][8];
-#pragma unroll
-  for (int q = 0; q < RB; ++q)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) acc[q][j] = 0.f;
-  auto fma8 = [&](const u32x4 w, int r) {
-    float f[8];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      f[2 * j] = __uint_as_float(w[j] << 16);
-      f[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
-    }
-#pragma unroll
-    for (int q = 0; q < RB; ++q) {
-      if (q < nrow) {
-        const float aq = sa[q * rv + r];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc[q][j] = fmaf(aq, f[j], acc[q][j]);
-      }
-    }
-  };
-  for (int r = rg; r < rv; r += 64 * U) {
-    u32x4 cur[U];
-#pragma unroll
-    for (int k = 0; k < U; ++k) cur[k] = v[k];
-    if (r + 64 * U < rv) issue(r + 64 * U);    // next batch in flight while this one multiplies
-#pragma unroll
-    for (int k = 0; k < U; ++k)
-      if (r + 64 * k < rv) fma8(cur[k], r + 64 * k);
-  }
-  // one reduction round: every thread's 8 rows x 8 columns go to LDS, then
-  // each of the 256 outputs sums its 64 rank groups in order
-  float* red = sa + RB * rv;                   // [64 rank groups][RB rows][32 columns]
-  __syncthreads();
-#pragma unroll
-  for (int q = 0; q < RB; ++q)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) red[(rg * RB + q) * 32 + 8 * c8 + j] = acc[q][j];
-  __syncthreads();
-  {
-    const int q = tid / 32, cc = tid % 32;
-    if (q < nrow && ct * 32 + cc < dh) {
-      float t = 0.f;
-      for (int k = 0; k < 64; ++k) t += red[(k * RB + q) * 32 + cc];
-      const int row = row0 + q;
-      const int b = row / qpk, h = kv * qpk + row % qpk;
-      out[(int64_t(b) * tb.n_q_heads + h) * dh + ct * 32 + cc] = t;
-    }
-  }
-}
-
 template <int W, int NT, int MTW, int KR>
 hipError_t launch_split(const dckv_plan& p, const DecodeShape& sh, const u32x4* qblk,
                         const void* pool, int64_t num_pages, const int32_t* page_table,
@@ -954,18 +848,19 @@ hipError_t launch_merge_upproj(const dckv_plan& p, const DecodeShape& sh, const 
                        sh.n_split, p.rv, amerged, p.tables, p.mfma);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int rows = sh.batch * p.Q * p.qpk;            // (sequence, query, head of a KV head)
-  const size_t lds_up = (size_t(8) * p.rv + 64 * 8 * 32) * sizeof(float);
-  e = hipFuncSetAttribute(reinterpret_cast<const void*>(upproj),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, int(lds_up));
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(upproj, dim3((rows + 7) / 8, p.Hkv, (p.dh + 31) / 32), dim3(256), lds_up,
-                     stream, amerged, static_cast<const bf16*>(R_value), out, sh.batch * p.Q,
-                     p.rv, p.tables);
-  return hipGetLastError();
+  return launch_upproj(p, sh.batch * p.Q, amerged, R_value, out, stream);
 }
 
 }  // namespace
+
+hipError_t launch_fold(const dckv_plan& p, const MfmaTables& mt, int32_t batch, const float* q,
+                       const void* R_keys, void* qblk, hipStream_t stream) {
+  const float scale = kLog2e / std::sqrt(float(p.dh));
+  hipLaunchKernelGGL(fold_blocks, dim3(batch * mt.n_slices, 16, mt.max_pairs), dim3(64), 0, stream, q,
+                     static_cast<const bf16*>(R_keys), static_cast<u32x4*>(qblk), scale, p.tables,
+                     mt);
+  return hipGetLastError();
+}
 
 size_t mfma_split_lds_bytes(const dckv_plan& p) {
   return size_t(p.mfma.max_pairs) * 2048 + 32 * kPStride * 2 + 2 * 8 * 32 * 4 + kPageSlots * 4;
@@ -985,10 +880,7 @@ hipError_t launch_decode_mfma(const dckv_plan& p, const DecodeShape& sh, const f
   float* part = reinterpret_cast<float*>(ws + sh.off_acc);
   float* amerged = reinterpret_cast<float*>(ws + sh.off_opart);
   const size_t lds = mfma_split_lds_bytes(p);
-  const float scale = kLog2e / std::sqrt(float(p.dh));
-  hipLaunchKernelGGL(fold_blocks, dim3(sh.batch * p.mfma.n_slices, 16, p.mfma.max_pairs), dim3(64),
-                     0, stream, q, static_cast<const bf16*>(R_keys), qt, scale, p.tables, p.mfma);
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_fold(p, p.mfma, sh.batch, q, R_keys, qt, stream);
   if (e != hipSuccess) return e;
   if (p.mfma.waves == 4)
     e = p.mfma.nt == 1

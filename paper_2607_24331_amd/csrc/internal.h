@@ -81,15 +81,25 @@ struct DecodeShape {
   int32_t max_context;
   int32_t split_tokens;
   int32_t n_split;          // ceil(max_context / split_tokens), at least 1
-  bool mfma;                // bf16 MFMA path (else the portable VALU path)
+  bool mfma;                // bf16 single-pass MFMA path (split_mfma)
+  bool pass;                // bf16 two-pass MFMA path (score_pages, value_pages)
   int32_t n_units;          // batch * n_split rounded up to a multiple of 8: grid units (MFMA path)
   int32_t n_rchunks;        // value-rank chunks of the merge (MFMA path)
+  // two-pass path
+  int32_t npm;              // pages of the longest sequence: ceil(max_context / 64), at least 1
+  int32_t unit_pages;       // pages a score work-group
+  int32_t units_per_seq;    // score work-groups a sequence
+  int32_t chunk_pages;      // pages a value chunk
+  int32_t n_chunks;         // value chunks a sequence
+  int32_t rgt;              // 16-rank value tiles a value work-group: 4, 6 or 8
+  int32_t n_rgroups;        // value rank groups: ceil(r_v / (16 rgt))
   size_t off_qt;            // workspace byte offsets
-  size_t off_ml;
-  size_t off_acc;
-  size_t off_opart;
+  size_t off_ml;            // (m, l) of splits; two-pass: (E, L) of chunks
+  size_t off_acc;           // split accumulators; two-pass: chunk accumulators
+  size_t off_opart;         // merged value-latent rows
   size_t off_rt;            // rotary decode: transposed key factors
-  size_t off_p;             // rotary decode: softmax weights of each split (bf16)
+  size_t off_p;             // softmax weights (bf16): rotary splits; two-pass pages
+  size_t off_el;            // two-pass: per-page (e, l) records
   size_t bytes;
 };
 
@@ -106,13 +116,17 @@ struct DenseShape {
 
 struct dckv_plan {
   int32_t m, Hq, Hkv, dh, G, rv, dtype, split_tokens, head_slices, decode_waves, Q;
+  int32_t decode_passes;             // 0 per call, 1 single-pass, 2 two-pass
   int32_t RK, RKp, rvp, qpk, qlen;
   int64_t page_elems, value_base, key_factor_elems;
   std::vector<int32_t> group_of_kv, ranks, hg, pos_in_group, koff, qoff;
   std::vector<int64_t> roff;
   dckv::HeadTables tables;
-  bool mfma_ok = false;              // bf16 MFMA decode path applies
+  bool mfma_ok = false;              // bf16 single-pass MFMA decode path applies
   dckv::MfmaTables mfma{};
+  bool pass_ok = false;              // bf16 two-pass decode applies (one query, <= 32 heads)
+  dckv::MfmaTables pass{};           // its tables: one slice, group order by fewest chunk loads
+  int32_t pass_ring = 0;             // score-pass loads in flight a wave (16 or 32)
   int32_t key_chunk_loads = 0;       // key chunks the MFMA tiles load a page
   dckv::RopeTables rope{};           // rotary decode tables (valid with mfma_ok)
   int64_t rope_rt_elems = 0;         // elements of the transposed key factors
@@ -141,6 +155,24 @@ int check_decode(const char* where, const dckv_plan* p, const float* q, int32_t 
 
 // Builds plan.mfma and sets plan.mfma_ok (host only, no HIP call).
 void build_mfma_tables(dckv_plan& p);
+
+// Builds plan.pass and sets plan.pass_ok (host only, no HIP call).
+void build_pass_tables(dckv_plan& p);
+
+// Two-pass decode (decode_pass.hip).
+size_t pass_score_lds_bytes(const dckv_plan& p);
+size_t pass_value_lds_bytes(const dckv_plan& p, int rgt);
+int pass_max_chunk_pages();
+hipError_t launch_decode_pass(const dckv_plan& p, const DecodeShape& sh, const float* q,
+                              const void* pool, int64_t num_pages, const int32_t* page_table,
+                              int32_t max_pages, const int32_t* seq_lens, const void* R_keys,
+                              const void* R_value, float* out, void* workspace, hipStream_t stream);
+// o = a R_v for batch_rows (sequence, query) rows of merged value-latent rows.
+hipError_t launch_upproj(const dckv_plan& p, int32_t batch_rows, const float* amerged,
+                         const void* R_value, float* out, hipStream_t stream);
+// Folded-query MFMA operand blocks (decode_mfma.hip) for the tables `mt`.
+hipError_t launch_fold(const dckv_plan& p, const MfmaTables& mt, int32_t batch, const float* q,
+                       const void* R_keys, void* qblk, hipStream_t stream);
 
 // MFMA decode path (decode_mfma.hip).
 size_t mfma_split_lds_bytes(const dckv_plan& p);

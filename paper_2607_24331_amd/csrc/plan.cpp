@@ -115,6 +115,18 @@ void build_mfma_tables(dckv_plan& p) {
   MfmaTables& t = p.mfma;
   const int32_t nrows = p.Q * p.Hq;
   int32_t J = p.head_slices > 0 ? p.head_slices : (nrows + kSliceHeads - 1) / kSliceHeads;
+  t.mt_v = (p.rv + 15) / 16;
+  // Eight waves (two a SIMD, so one wave's loads overlap the other's MFMAs)
+  // whenever every wave gets at least one 16-rank value tile; four waves
+  // for very small value ranks.  Accumulators take nt * mtw * 4 registers:
+  // beyond 128 a lane, a default slicing takes twice the slices (16 rows a
+  // slice), each slice then reading the value part on its own.
+  t.waves = p.decode_waves ? p.decode_waves : (t.mt_v >= 8 ? 8 : 4);
+  t.mtw = (t.mt_v + t.waves - 1) / t.waves;
+  if (p.head_slices == 0) {
+    while (J < kMaxSlices && J < nrows && ((nrows + J - 1) / J + 15) / 16 * t.mtw > 32) J *= 2;
+    J = std::min(J, kMaxSlices);
+  }
   if (J > kMaxSlices || J > nrows) return;
   const int32_t per = (nrows + J - 1) / J;
   if (per > kSliceHeads) return;
@@ -122,12 +134,6 @@ void build_mfma_tables(dckv_plan& p) {
   t.q_heads = p.Hq;
   t.queries = p.Q;
   t.nt = (per + 15) / 16;
-  t.mt_v = (p.rv + 15) / 16;
-  // Eight waves (two a SIMD, so one wave's loads overlap the other's MFMAs)
-  // whenever every wave gets at least one 16-rank value tile; four waves
-  // for very small value ranks.  Accumulators take nt * mtw * 4 registers.
-  t.waves = p.decode_waves ? p.decode_waves : (t.mt_v >= 8 ? 8 : 4);
-  t.mtw = (t.mt_v + t.waves - 1) / t.waves;
   if (t.nt * t.mtw > 32) return;               // beyond 128 accumulator registers a lane
   t.mtw_t = 0;
   for (int32_t c : {6, 8, 12, 16, 32})
@@ -174,6 +180,47 @@ void build_mfma_tables(dckv_plan& p) {
   const int64_t lds = int64_t(t.max_pairs) * 2048 + 32 * 72 * 2 + 2 * 8 * 32 * 4 + 256 * 4;
   if (lds > 160 * 1024) return;
   p.mfma_ok = true;
+}
+
+// Tables of the two-pass decode: one query a sequence and at most 32 query
+// heads, all in one slice of one or two 16-row tiles.  The score pass loads,
+// a page, the key chunks of each tile's groups, so the group order is the
+// one with the fewest chunk loads (every order for up to seven groups, else
+// the group-id order; ties keep the earlier order).  Any value rank: the
+// value pass takes 16-rank tiles in groups of 4, 6 or 8 (chosen per call).
+void build_pass_tables(dckv_plan& p) {
+  p.pass_ok = false;
+  p.pass = MfmaTables{};
+  p.pass_ring = 0;
+  if (p.dtype != DCKV_BF16 || p.dh % 8 != 0 || p.Q != 1 || p.Hq > kSliceHeads) return;
+  if (p.head_slices > 1 || p.decode_waves == 4) return;   // explicit single-pass shapes
+  MfmaTables& t = p.pass;
+  t.n_slices = 1;
+  t.q_heads = p.Hq;
+  t.queries = 1;
+  t.nt = (p.Hq + 15) / 16;
+  t.mt_v = (p.rv + 15) / 16;
+  t.waves = 8;
+  std::vector<std::vector<int32_t>> rows_of(p.G);
+  for (int32_t h = 0; h < p.Hq; ++h) rows_of[p.group_of_kv[h / p.qpk]].push_back(h);
+  std::vector<int32_t> gorder(p.G);
+  for (int32_t g = 0; g < p.G; ++g) gorder[g] = g;
+  const bool search = p.G <= 7;
+  MfmaTables cand = t, best = t;
+  int32_t best_total = -1;
+  do {
+    int32_t total = 0;
+    if (!place_rows(p, rows_of, gorder, 1, p.Hq, cand, &total)) continue;
+    if (best_total < 0 || total < best_total) {
+      best = cand;
+      best_total = total;
+    }
+  } while (search && std::next_permutation(gorder.begin(), gorder.end()));
+  if (best_total < 0) return;
+  t = best;
+  p.pass_ring = 16;                            // score-pass loads in flight a wave
+  if (pass_score_lds_bytes(p) > 160 * 1024 || pass_value_lds_bytes(p, 8) > 160 * 1024) return;
+  p.pass_ok = true;
 }
 
 // Tables of the rotary decode: per KV head its group's key columns and
@@ -271,6 +318,8 @@ int dckv_plan_create(const dckv_layer_desc* d, dckv_plan** out) {
                 d->split_tokens, DCKV_PAGE_TOKENS);
   if (d->decode_waves != 0 && d->decode_waves != 4 && d->decode_waves != 8)
     return fail(DCKV_EINVAL, "plan_create: decode_waves %d is not 0, 4 or 8", d->decode_waves);
+  if (d->decode_passes < 0 || d->decode_passes > 2)
+    return fail(DCKV_EINVAL, "plan_create: decode_passes %d is not 0, 1 or 2", d->decode_passes);
   if (d->head_slices < 0 || d->head_slices > DCKV_MAX_HEADS)
     return fail(DCKV_EINVAL, "plan_create: head_slices %d outside [0,%d]", d->head_slices,
                 DCKV_MAX_HEADS);
@@ -312,6 +361,7 @@ int dckv_plan_create(const dckv_layer_desc* d, dckv_plan** out) {
     p->split_tokens = d->split_tokens;
     p->head_slices = d->head_slices;
     p->decode_waves = d->decode_waves;
+    p->decode_passes = d->decode_passes;
     p->Q = d->queries_per_seq > 0 ? d->queries_per_seq : 1;
     p->group_of_kv.assign(d->group_of_kv_head, d->group_of_kv_head + Hkv);
     p->ranks.assign(d->group_rank, d->group_rank + G);
@@ -365,7 +415,14 @@ int dckv_plan_create(const dckv_layer_desc* d, dckv_plan** out) {
     return fail(DCKV_ENOMEM, "plan_create: host allocation failed");
   }
   dckv::build_mfma_tables(*p);
+  dckv::build_pass_tables(*p);
   dckv::build_rope_tables(*p);
+  if (p->decode_passes == 2 && !p->pass_ok) {
+    delete p;
+    return fail(DCKV_EINVAL, "plan_create: decode_passes 2 needs bf16 latents, one query a sequence, "
+                "at most 32 query heads and d_h a multiple of 8");
+  }
+  if (p->decode_passes == 1) p->pass_ok = false;
   *out = p;
   return DCKV_OK;
 }
@@ -392,7 +449,8 @@ int dckv_plan_info(const dckv_plan* p, dckv_plan_geometry* geo, int32_t* koff,
     geo->q_per_kv = p->qpk;
     geo->folded_query_len = p->qlen;
     geo->split_tokens = p->split_tokens;
-    geo->mfma_path = p->mfma_ok ? 1 : 0;
+    geo->mfma_path = (p->mfma_ok || p->pass_ok) ? 1 : 0;
+    geo->two_pass = p->pass_ok ? 1 : 0;
     geo->head_slices = p->mfma_ok ? p->mfma.n_slices : 0;
     geo->queries_per_seq = p->Q;
     geo->decode_waves = p->mfma_ok ? p->mfma.waves : 0;

@@ -43,7 +43,7 @@ class Plan:
     def __init__(self, hidden: int, num_q_heads: int, num_kv_heads: int, head_dim: int,
                  group_of_kv_head: Sequence[int], group_rank: Sequence[int], value_rank: int,
                  dtype: str = "bf16", split_tokens: int = 0, head_slices: int = 0,
-                 decode_waves: int = 0, queries_per_seq: int = 1):
+                 decode_waves: int = 0, queries_per_seq: int = 1, decode_passes: int = 0):
         if dtype not in _DTYPES:
             raise ValueError(f"dtype must be one of {sorted(_DTYPES)}")
         self.dtype = dtype
@@ -54,7 +54,7 @@ class Plan:
                               ctypes.cast(self._gmap, ctypes.POINTER(ctypes.c_int32)),
                               ctypes.cast(self._ranks, ctypes.POINTER(ctypes.c_int32)),
                               value_rank, _DTYPES[dtype][0], split_tokens, head_slices,
-                              queries_per_seq, decode_waves)
+                              queries_per_seq, decode_waves, decode_passes)
         handle = ctypes.c_void_p()
         _check(_lib.dckv_plan_create(ctypes.byref(desc), ctypes.byref(handle)), "plan_create")
         self._handle = handle

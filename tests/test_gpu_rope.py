@@ -50,8 +50,10 @@ def _run(inp, plan, pool, base, max_context=None):
 
 
 # (case, base): the position-free decode's small cases that take the MFMA path
+# (valu_bf16: value rank 2304 over 32 heads, two row slices of 16 heads)
 CASES = [("mha_odd", 10000.0), ("gqa_uneven", 10000.0), ("single_group", 100.0),
-         ("singletons", 500000.0), ("mha32_two_tiles", 10000.0), ("gqa_reordered", 1000.0)]
+         ("singletons", 500000.0), ("mha32_two_tiles", 10000.0), ("gqa_reordered", 1000.0),
+         ("valu_bf16", 10000.0)]
 
 
 @pytest.mark.parametrize("name, base", CASES)
@@ -152,12 +154,12 @@ def test_rope_full_size_sampled_rows(name, n_rows):
 
 def test_rope_rejects_plans_off_its_path():
     from paper_2607_24331_amd import DckvError, Plan, decode_rope
-    wl, inp, split = _small_inputs("valu_bf16")         # value rank beyond the MFMA accumulators
+    wl, inp, split = _small_inputs("mha_odd", "f32")    # fp32 latents: the portable kernels
     plan = plan_for(wl, split)
     assert plan.geometry["mfma_path"] == 0
     pool = plan.new_pool(4)
     with pytest.raises(DckvError, match="MFMA"):
         decode_rope(plan, torch.zeros(1, wl.num_q_heads, wl.head_dim).cuda(), pool,
                     torch.zeros(1, 4, dtype=torch.int32).cuda(), torch.ones(1, dtype=torch.int32).cuda(),
-                    64, torch.zeros(plan.key_factor_elems, dtype=torch.bfloat16).cuda(),
-                    torch.zeros(wl.value_rank, wl.num_kv_heads * wl.head_dim, dtype=torch.bfloat16).cuda())
+                    64, torch.zeros(plan.key_factor_elems, dtype=plan.torch_dtype).cuda(),
+                    torch.zeros(wl.value_rank, wl.num_kv_heads * wl.head_dim, dtype=plan.torch_dtype).cuda())

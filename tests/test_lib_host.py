@@ -107,12 +107,15 @@ def test_plan_create_rejects(lib, change, status):
 
 
 def test_workspace_bytes_grows_with_work():
+    from paper_2607_24331_amd import Plan
     wl = make_workload("gqa8b_b4_t32k")
-    p = _plan(wl)
-    a = p.workspace_bytes(4, 32768)
-    assert a > p.workspace_bytes(1, 32768) > 0
-    assert a >= p.workspace_bytes(4, 1024)
-    assert p.workspace_bytes(4, 0) > 0
+    for passes in (1, 2):                 # either kernel set, chosen for every call
+        p = Plan(wl.hidden, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_of_kv,
+                 wl.group_rank, wl.value_rank, wl.dtype, decode_passes=passes)
+        a = p.workspace_bytes(4, 32768)
+        assert a > p.workspace_bytes(1, 32768) > 0
+        assert a >= p.workspace_bytes(4, 1024)
+        assert p.workspace_bytes(4, 0) > 0
 
 
 @pytest.mark.skipif(torch.cuda.is_available(), reason="raw fake pointers are only passed on a host without a GPU")
@@ -197,9 +200,23 @@ def test_decode_path_selection():
     for name, mfma in expect.items():
         assert _plan(make_workload(name)).geometry["mfma_path"] == mfma, name
     from paper_2607_24331_amd import Plan
-    # value rank 2304 with 32 heads exceeds the MFMA accumulators: portable path
-    p = Plan(2560, 32, 32, 128, [i // 8 for i in range(32)], [300, 200, 100, 50], 2304, "bf16")
-    assert p.geometry["mfma_path"] == 0
+    # value rank 2304 with 32 heads: the two-pass kernels take any value rank;
+    # the single-pass kernel takes two slices of 16 rows (its accumulators
+    # hold 2304 ranks for 16 rows a slice, not 32)
+    args = (2560, 32, 32, 128, [i // 8 for i in range(32)], [300, 200, 100, 50], 2304, "bf16")
+    p = Plan(*args)
+    assert p.geometry["mfma_path"] == 1 and p.geometry["two_pass"] == 1
+    assert p.geometry["head_slices"] == 2
+    # value rank 4096, 32 heads, 4 queries a sequence: eight slices of 16 rows
+    p4 = Plan(4096, 32, 32, 128, [i // 8 for i in range(32)], [300, 200, 100, 50], 4096, "bf16",
+              queries_per_seq=4)
+    assert p4.geometry["mfma_path"] == 1 and p4.geometry["two_pass"] == 0
+    assert p4.geometry["head_slices"] == 8
+    # an explicit single-pass plan, and a two-pass request the layer cannot take
+    assert Plan(*args, decode_passes=1).geometry["two_pass"] == 0
+    from paper_2607_24331_amd import DckvError
+    with pytest.raises(DckvError, match="decode_passes"):
+        Plan(*args, queries_per_seq=2, decode_passes=2)
     # explicit head slices
     wl = make_workload("mha_long_t128k")
     from paper_2607_24331_amd import Plan as P2
