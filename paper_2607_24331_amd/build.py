@@ -52,13 +52,25 @@ def _run(cmd, verbose):
         print(out)
 
 
-def build(verbose: bool = False) -> str:
+# Host code checked by AddressSanitizer and UndefinedBehaviorSanitizer (the
+# kernels are built as usual); load it with DCKV_LIBRARY and the sanitizer
+# runtime preloaded, e.g.
+#   DCKV_LIBRARY=paper_2607_24331_amd/libdckv_sanitized.so \
+#   LD_PRELOAD=$(g++ -print-file-name=libasan.so) ASAN_OPTIONS=detect_leaks=0 \
+#   python -m pytest tests/test_lib_host.py tests/test_lib_offline_host.py
+SANITIZE_FLAGS = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                  "-fno-sanitize-recover=all"]
+SANITIZED_LIB = os.path.join(PKG, "libdckv_sanitized.so")
+
+
+def build(verbose: bool = False, sanitize: bool = False) -> str:
     hipcc = shutil.which("hipcc") or os.path.join(ROCM, "bin", "hipcc")
     os.makedirs(BUILD, exist_ok=True)
     objs = []
     for src in HOST_SOURCES:
-        obj = os.path.join(BUILD, src + ".o")
-        _run(["g++", *HOST_FLAGS, "-I", INCLUDE, "-I", CSRC, "-I", os.path.join(ROCM, "include"),
+        obj = os.path.join(BUILD, src + (".san.o" if sanitize else ".o"))
+        flags = HOST_FLAGS + (SANITIZE_FLAGS if sanitize else [])
+        _run(["g++", *flags, "-I", INCLUDE, "-I", CSRC, "-I", os.path.join(ROCM, "include"),
               "-c", os.path.join(CSRC, src), "-o", obj], verbose)
         objs.append(obj)
     for src in HIP_SOURCES:
@@ -66,11 +78,17 @@ def build(verbose: bool = False) -> str:
         _run([hipcc, *HIPCC_FLAGS, *HIPCC_EXTRA.get(src, []), "-I", INCLUDE, "-I", CSRC, "-c",
               os.path.join(CSRC, src), "-o", obj], verbose)
         objs.append(obj)
-    tmp = LIB + ".tmp"
-    _run([hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, *objs], verbose)
-    os.replace(tmp, LIB)
-    return LIB
+    lib = SANITIZED_LIB if sanitize else LIB
+    tmp = lib + ".tmp"
+    if sanitize:   # g++ links the sanitizer runtimes its host objects were built for
+        _run(["g++", "-shared", "-fPIC", *SANITIZE_FLAGS, "-o", tmp, *objs,
+              "-L", os.path.join(ROCM, "lib"), "-lamdhip64", f"-Wl,-rpath,{os.path.join(ROCM, 'lib')}"],
+             verbose)
+    else:
+        _run([hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, *objs], verbose)
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, sanitize="--sanitize" in sys.argv))

@@ -10,7 +10,9 @@ import ctypes
 import os
 import re
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdckv.so")
+# DCKV_LIBRARY selects another build of the same library (the sanitized one)
+LIB_PATH = os.environ.get("DCKV_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                                                          "libdckv.so")
 HEADER_PATH = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
                            "include", "dckv.h")
 
