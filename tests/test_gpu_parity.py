@@ -363,11 +363,98 @@ def test_full_workload_sampled_rows(name):
             rounded = obf16.round_to_bf16(exact)
             bound = obf16.ulp_bf16(rounded) + wl.hidden * 2.0 ** -24 * oappend.abs_bound(inp.x, L)
             assert np.all(np.abs(Zg - rounded) <= bound)
-    pairs = sample_pairs(wl, 8 if wl.seq_lens[0] < 100000 else 5)
+    if wl.batch >= 32:
+        pairs = every_sequence_pairs(wl)         # one head of every sequence, every group
+    else:
+        pairs = sample_pairs(wl, 8 if wl.seq_lens[0] < 100000 else 5)
     ref = oracle_rows(inp, pairs)
     errs = [row_rel_err(out[b, h], ref[(b, h)]) for b, h in pairs]
     _report(name, errs)
     assert max(errs) <= TOL_REL_ROW
+
+
+def every_sequence_pairs(wl):
+    """One (sequence, head) row of every sequence; sequence b takes a head of
+    group b mod G (the group's heads in turn), so every group is covered."""
+    qpk = wl.num_q_heads // wl.num_kv_heads
+    members = [[kv for kv in range(wl.num_kv_heads) if wl.group_of_kv[kv] == g]
+               for g in range(wl.num_groups)]
+    pairs = []
+    for b in range(wl.batch):
+        g = b % wl.num_groups
+        kv = members[g][(b // wl.num_groups) % len(members[g])]
+        pairs.append((b, kv * qpk + (b % qpk)))
+    assert {wl.group_of_kv[h // qpk] for _, h in pairs} == set(range(wl.num_groups))
+    return pairs
+
+
+def test_multi_query_long_layer_benchmarked_shape():
+    # the long-context layer with 4 causal queries a sequence, in the launch
+    # shape the benchmark times (4 row slices, 2048-token splits); rows of
+    # two heads (different groups) for every query, query 0 included
+    from paper_2607_24331_amd import Plan, decode
+    wl = make_workload("mha_long_t128k")
+    print("[parity] start mha_long_t128k Q=4", flush=True)
+    inp = make_inputs(wl)
+    Q = 4
+    plan = Plan(wl.hidden, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_of_kv,
+                wl.group_rank, wl.value_rank, wl.dtype, 2048, queries_per_seq=Q)
+    geo = plan.geometry
+    assert geo["mfma_path"] == 1 and geo["head_slices"] == 4 and geo["two_pass"] == 0
+    pool = gpu_pool_with_append(inp, plan)
+    qm = np.random.default_rng(12).standard_normal(
+        (wl.batch, Q, wl.num_q_heads, wl.head_dim)).astype(np.float32)
+    out = decode(plan, torch.from_numpy(qm).cuda(), pool, torch.from_numpy(inp.page_table).cuda(),
+                 torch.from_numpy(inp.seq_lens).cuda(), int(max(wl.seq_lens)),
+                 dev(inp.R_keys_flat, wl.dtype), dev(inp.R_value, wl.dtype))
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().astype(np.float64)
+    assert np.isfinite(got).all()
+    from gpu_common import seq_latents
+    bk = book_for(wl)
+    Zk, Zv = seq_latents(inp, 0)
+    T = wl.seq_lens[0]
+    heads = sample_pairs(wl, 2, seed=4)[:2]
+    errs = []
+    for _, h in heads:
+        K, V = oattn.rebuild(Zk, Zv, inp.R_blocks, inp.R_value, bk, h)   # once a head
+        for i in range(Q):
+            n = oattn.visible_tokens(T, Q, i)
+            ref = oattn.attend(qm[0, i, h], K[:n], V[:n])
+            errs.append(row_rel_err(got[0, i, h], ref))
+        del K, V
+    _report("mha_long_t128k/Q4", errs)
+    assert max(errs) <= TOL_REL_ROW
+
+
+def test_value_rank_3072_full_layer_both_kernel_sets():
+    # a full-size MHA layer (4 x 32768 tokens) with value rank 3072: the
+    # single-pass kernel needs two row slices, the two-pass kernels one
+    from paper_2607_24331_amd import Plan
+    wl = custom_workload(name="mha_rv3072_b4_t32k", seed=3072, hidden=4096, num_q_heads=32,
+                         num_kv_heads=32, head_dim=128, group_of_kv=_groups((8, 6, 6, 5, 4, 3), 5),
+                         group_rank=(400, 300, 300, 240, 200, 96), value_rank=3072, dtype="bf16",
+                         batch=4, seq_lens=(32768, 32768, 30000, 32768),
+                         prefill_lens=(32768, 32768, 30000, 32768), factor_scheme="orthonormal")
+    print("[parity] start mha_rv3072_b4_t32k", flush=True)
+    inp = make_inputs(wl)
+    pairs = sample_pairs(wl, 6, seed=9)
+    ref = oracle_rows(inp, pairs)
+    outs = []
+    for passes in (1, 0):
+        plan = Plan(wl.hidden, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_of_kv,
+                    wl.group_rank, wl.value_rank, wl.dtype, decode_passes=passes)
+        geo = plan.geometry
+        assert geo["mfma_path"] == 1 and geo["head_slices"] == 2
+        pool = gpu_pool_with_append(inp, plan)
+        out = run_decode(inp, plan, pool)
+        assert np.isfinite(out).all()
+        errs = [row_rel_err(out[b, h], ref[(b, h)]) for b, h in pairs]
+        _report(f"mha_rv3072/{'single-pass' if passes == 1 else 'default (two-pass)'}", errs)
+        assert max(errs) <= TOL_REL_ROW
+        outs.append(out)
+        del pool
+    assert np.max(np.abs(outs[0] - outs[1])) <= 1e-2 * np.max(np.abs(outs[0]))
 
 
 @pytest.mark.parametrize("hidden", [200, 320, 384, 512])
