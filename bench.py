@@ -11,9 +11,17 @@ summing to 1536, value rank 2048, bf16 latents.
 
 Prints one JSON line.  `value` is decode tokens/s (sequences decoded per
 second of step time) with every input resident in HBM before timing starts.
-`roofline` covers the split-K attention kernel, timed with HIP events
-recorded around each of its launches on the decode stream.  `cpu_baseline`
-times the fp64 CPU oracle on a bounded sample of the same workload.
+`roofline` covers the dominant kernel (the split-K attention kernel, or the
+value pass when a call takes the two-pass kernels), timed with HIP events
+stamped by its own dispatch; `decode_call` is the whole decode call (fold,
+attention, merge, up-projection) against the same peak; `copy_peak` is a
+2 GiB device copy timed the same way, a measured second denominator.
+`cpu_baseline` times the fp64 CPU oracle on a bounded sample of the same
+workload.  Latent pools are touched in turn (`pool_copies`) so that more
+than 512 MB pass between two reads of one pool: the 256 MB last-level cache
+cannot serve them.  With the default workload the GQA layer (4 sequences x
+32768 tokens) is timed in the same run and reported under `also`, with its
+own step time, roofline, decode call and CPU baseline.
 """
 
 from __future__ import annotations
@@ -47,6 +55,13 @@ def parse():
                     help="causal queries a sequence in each decode (speculative verification / "
                          "chunked prefill); 1 is plain decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--also", default="auto",
+                    help="a second workload timed in the same run and reported under 'also' "
+                         "(auto: the GQA layer when the default long-context layer is timed; "
+                         "none: no second workload)")
+    ap.add_argument("--pool-copies", type=int, default=0,
+                    help="latent pool copies touched in turn (0: enough for > 512 MB a rotation, "
+                         "so steps stream from HBM rather than the 256 MB last-level cache)")
     ap.add_argument("--decode-only", action="store_true",
                     help="time the decode alone (no latent append in the step)")
     ap.add_argument("--dense", action="store_true",
@@ -217,7 +232,8 @@ def algorithmic_bytes(wl):
     if wl.append_tokens:
         R = wl.key_rank_total + wl.value_rank
         append = (wl.append_tokens * wl.hidden + wl.hidden * R + wl.append_tokens * R) * s
-    return dict(latent=latent, factors=factors, q_out=qo, append=append,
+    value_latent = ctx * wl.value_rank * s
+    return dict(latent=latent, value_latent=value_latent, factors=factors, q_out=qo, append=append,
                 decode_total=latent + factors + qo)
 
 
@@ -438,7 +454,7 @@ def main():
         sys.exit(2)
     import torch
     sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
-    from paper_2607_24331_amd import Plan, decode, decode_rope, latent_append
+    import paper_2607_24331_amd  # noqa: F401  (fails loudly when the library is not built)
     from workloads import make_workload
 
     if args.offline:
@@ -446,6 +462,50 @@ def main():
     wl = make_workload(args.workload)
     if args.dense:
         return main_dense(args, torch, wl)
+    copy = copy_peak(torch)
+    rec = bench_compressed(args, torch, wl, copy)
+    also = args.also
+    if also == "auto":
+        also = ("gqa8b_b4_t32k" if args.workload == "mha_long_t128k" and args.queries == 1
+                and args.rope is None else "none")
+    if also != "none":
+        sub = bench_compressed(args, torch, make_workload(also), copy)
+        for k in ("metric", "n_gpus", "higher_is_better", "scaling", "vs_baseline", "data", "warmup"):
+            sub.pop(k, None)
+        rec["also"] = {also: sub}
+    print(json.dumps(rec), flush=True)
+
+
+def copy_peak(torch, gib=2, reps=10):
+    """Device-to-device copy of `gib` GiB timed with HIP events: the bytes read
+    plus written over the time, a measured second denominator beside the
+    published 8 TB/s."""
+    n = gib << 30
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    del src, dst
+    torch.cuda.empty_cache()
+    gbs = 2.0 * n / (ms * 1e-3) / 1e9
+    print(f"[bench] device copy of {gib} GiB: {ms:.3f} ms, {gbs:.0f} GB/s (read + write)",
+          file=sys.stderr, flush=True)
+    return {"gbs": gbs, "bytes_read_and_written": 2 * n, "ms": ms,
+            "kind": f"device-to-device copy of {gib} GiB (torch copy_), read + written bytes / time"}
+
+
+def bench_compressed(args, torch, wl, copy):
+    """Time the compressed-KV step on one workload; returns its JSON record."""
+    from paper_2607_24331_amd import Plan, decode, decode_rope, latent_append
+    from workloads.inputs import random_pool_fill
     plan = Plan(wl.hidden, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_of_kv,
                 wl.group_rank, wl.value_rank, wl.dtype, args.split_tokens, args.head_slices,
                 args.decode_waves, args.queries, args.decode_passes)
@@ -453,28 +513,36 @@ def main():
     Q = args.queries
     inp = device_inputs(wl, plan, torch, Q)
     max_ctx = max(wl.seq_lens)
-    split_used = plan.split_tokens or _auto_split(plan, wl, max_ctx)
+    info = plan.launch_info(wl.batch, max_ctx)
+    split_used = info["split_tokens"]
     out = torch.empty(tuple(inp["q"].shape), dtype=torch.float32, device="cuda")
     rope = args.rope is not None
     if rope:
         if Q != 1 or not mfma:
             sys.exit("bench.py: --rope runs one query a sequence on the bf16 MFMA path")
-        split_used = min(split_used, 1024)            # the rotary decode's split cap
+        split_used = min(plan.split_tokens or _auto_split(plan, wl, max_ctx), 1024)
         ws = torch.empty(max(256, plan.rope_workspace_bytes(wl.batch, max_ctx)), dtype=torch.uint8,
                          device="cuda")
     else:
         ws = plan.new_workspace(wl.batch, max_ctx)
-
+    # Pool copies touched in turn, so that a step streams from HBM and not from
+    # the 256 MB last-level cache (MALL): enough copies for > 512 MB a rotation.
+    pool_bytes = wl.total_pages * plan.page_elems * wl.elem_bytes
+    copies = args.pool_copies or max(1, math.ceil(600e6 / pool_bytes))
+    pools = [inp["pool"]] + [random_pool_fill(wl.total_pages, plan.page_elems, wl.dtype,
+                                              seed=wl.seed + 100 * c, device="cuda")
+                             for c in range(1, copies)]
     append = bool(wl.append_tokens) and not args.decode_only
 
-    def step():
-        if append:
-            latent_append(plan, inp["x"], inp["L_keys"], inp["L_value"], inp["slot"], inp["pool"])
+    def step(k, with_append=True):
+        pool = pools[k % copies]
+        if append and with_append:
+            latent_append(plan, inp["x"], inp["L_keys"], inp["L_value"], inp["slot"], pool)
         if rope:
-            decode_rope(plan, inp["q"], inp["pool"], inp["page_table"], inp["seq_lens"], max_ctx,
+            decode_rope(plan, inp["q"], pool, inp["page_table"], inp["seq_lens"], max_ctx,
                         inp["R_keys"], inp["R_value"], rope_base=args.rope, out=out, workspace=ws)
         else:
-            decode(plan, inp["q"], inp["pool"], inp["page_table"], inp["seq_lens"], max_ctx,
+            decode(plan, inp["q"], pool, inp["page_table"], inp["seq_lens"], max_ctx,
                    inp["R_keys"], inp["R_value"], out=out, workspace=ws)
 
     if args.copy_calibration_mib:
@@ -484,10 +552,11 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    for _ in range(args.warmup):
-        step()
+    for k in range(args.warmup):
+        step(k)
     torch.cuda.synchronize()
-    print(f"[bench] {wl.name}: warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+    print(f"[bench] {wl.name}: warmup done ({args.warmup} steps, {copies} pool cop"
+          f"{'y' if copies == 1 else 'ies'})", file=sys.stderr, flush=True)
 
     K = args.steps
     every = max(1, args.profile_every)
@@ -507,26 +576,39 @@ def main():
             plan.set_profile_events(*ev[k])
         elif k - 1 in ev:
             plan.set_profile_events(None, None)
-        step()
+        step(k)
     t_end.record()
     torch.cuda.synchronize()
     plan.set_profile_events(None, None)
-    ms_total = t_start.elapsed_time(t_end)
-    ms_step = ms_total / K
+    ms_step = t_start.elapsed_time(t_end) / K
     kern_ms = sum(a.elapsed_time(b) for a, b in ev.values()) / len(ev)
-    print(f"[bench] timed {K} steps: {ms_step:.4f} ms/step, "
-          f"{'key-rebuild' if rope else 'split'} kernel {kern_ms:.4f} ms "
-          f"(HIP events on {len(ev)} of the {K} steps)",
-          file=sys.stderr, flush=True)
+    # the decode call alone (no append), same rotation of pools
+    if append:
+        t_start.record()
+        for k in range(K):
+            step(k, with_append=False)
+        t_end.record()
+        torch.cuda.synchronize()
+        ms_decode = t_start.elapsed_time(t_end) / K
+    else:
+        ms_decode = ms_step
+    two_pass = info["kernels"] == 2
+    print(f"[bench] {wl.name}: timed {K} steps: {ms_step:.4f} ms/step, decode call {ms_decode:.4f} ms, "
+          f"{'key-rebuild' if rope else ('value-pass' if two_pass else 'split')} kernel {kern_ms:.4f} ms "
+          f"(HIP events on {len(ev)} of the {K} steps)", file=sys.stderr, flush=True)
 
     nb = algorithmic_bytes(wl)
     launch = (f"split_tokens={split_used} head_slices={plan.geometry['head_slices']} "
               f"decode_waves={plan.geometry['decode_waves']}")
     if Q > 1:
         launch += f" queries_per_seq={Q}"
-    traffic = measured_traffic(wl, launch, Q) if mfma else None
-    achieved = nb["latent"] / (kern_ms * 1e-3) / 1e9
+    if two_pass:
+        launch = f"two_pass chunk_tokens={split_used}"
+    kernel_bytes = nb["value_latent"] if two_pass else nb["latent"]
+    traffic = measured_traffic(wl, launch, Q, "value_pages" if two_pass else "split_mfma") if mfma else None
+    achieved = kernel_bytes / (kern_ms * 1e-3) / 1e9
     value = wl.batch * Q / (ms_step * 1e-3)
+    decode_gbs = nb["decode_total"] / (ms_decode * 1e-3) / 1e9
     rec = {
         "metric": ("compressed-KV decode attention tokens/s (achieved HBM GB/s in roofline)" if Q == 1
                    else f"compressed-KV causal {Q}-query attention query tokens/s "
@@ -551,23 +633,32 @@ def main():
             "hidden": wl.hidden, "group_sizes": list(wl.group_sizes),
             "group_ranks": list(wl.group_rank), "value_rank": wl.value_rank,
             "latent_dtype": wl.dtype, "split_tokens": split_used,
-            "head_slices": plan.geometry["head_slices"],
+            "decode_kernels": ["portable", "single-pass", "two-pass"][info["kernels"]],
+            "head_slices": info["head_slices"],
             "decode_waves": plan.geometry["decode_waves"],
             "queries_per_seq": Q,
+            "pool_copies": copies, "pool_bytes": pool_bytes,
         },
         "context_tokens_per_s": sum(wl.seq_lens) / (ms_step * 1e-3),
         "step_hbm_gbs": (nb["decode_total"] + (nb["append"] if append else 0)) / (ms_step * 1e-3) / 1e9,
+        "decode_call": {
+            "ms": ms_decode, "bytes": nb["decode_total"], "hbm_gbs": decode_gbs,
+            "frac": decode_gbs / HBM_PEAK_GBS, "frac_of_copy_peak": decode_gbs / copy["gbs"],
+        },
+        "copy_peak": copy,
         "roofline": {
-            "kernel": "split-K latent attention (" + ("split_mfma" if mfma else "split_valu") + ")",
+            "kernel": ("value pass of the two-pass decode (value_pages)" if two_pass else
+                       "split-K latent attention (" + ("split_mfma" if mfma else "split_valu") + ")"),
             "bound": "hbm",
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
+            "frac_of_copy_peak": achieved / copy["gbs"],
             "traffic": traffic,
             "kernel_ms": kern_ms,
             "kernel_launches_timed": len(ev),
-            "bytes_per_launch": nb["latent"],
+            "bytes_per_launch": kernel_bytes,
             "launch": launch,
         },
     }
@@ -591,9 +682,11 @@ def main():
             "launch": f"split_tokens={split_used} rope",
         }
     if not args.no_cpu_baseline:
-        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        print(f"[bench] {wl.name}: timing the CPU oracle sample", file=sys.stderr, flush=True)
         rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, Q, append, args.rope)
-    print(json.dumps(rec), flush=True)
+    del pools, inp, ws
+    torch.cuda.empty_cache()
+    return rec
 
 
 if __name__ == "__main__":

@@ -183,6 +183,19 @@ int dckv_plan_info(const dckv_plan* plan, dckv_plan_geometry* geo, int32_t* koff
 int dckv_decode_workspace_bytes(const dckv_plan* plan, int32_t batch, int32_t max_context,
                                 size_t* bytes);
 
+/* The launch a dckv_decode call of `batch` sequences of at most
+ * `max_context` tokens takes: which kernels, and how the context is cut
+ * (it depends on the plan and these two numbers only). */
+typedef struct dckv_launch_info {
+  int32_t kernels;       /* 0 portable VALU kernels, 1 single-pass MFMA split kernel,
+                            2 two-pass MFMA kernels */
+  int32_t split_tokens;  /* context tokens a split (a value chunk on the two-pass path) */
+  int32_t n_split;       /* splits (chunks) of the longest sequence */
+  int32_t head_slices;   /* row slices of the single-pass kernel (1 otherwise) */
+} dckv_launch_info;
+int dckv_decode_launch_info(const dckv_plan* plan, int32_t batch, int32_t max_context,
+                            dckv_launch_info* info);
+
 /* Latent write for new tokens (Sec. III-A z = x L, per group L_g of Sec.
  * III-C and whole-projection L_v of Sec. III-D), computed with fp32
  * accumulation and rounded to nearest-even into the pool.

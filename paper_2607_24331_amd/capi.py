@@ -75,6 +75,15 @@ class PlanGeometry(ctypes.Structure):
     ]
 
 
+class LaunchInfo(ctypes.Structure):
+    _fields_ = [
+        ("kernels", ctypes.c_int32),
+        ("split_tokens", ctypes.c_int32),
+        ("n_split", ctypes.c_int32),
+        ("head_slices", ctypes.c_int32),
+    ]
+
+
 _vp = ctypes.c_void_p
 _i32 = ctypes.c_int32
 _i64 = ctypes.c_int64
@@ -86,6 +95,7 @@ SIGNATURES = {
     "dckv_plan_destroy": (None, [_vp]),
     "dckv_plan_info": (ctypes.c_int, [_vp, ctypes.POINTER(PlanGeometry), _pi32, _pi32, _pi32, _pi64]),
     "dckv_decode_workspace_bytes": (ctypes.c_int, [_vp, _i32, _i32, ctypes.POINTER(ctypes.c_size_t)]),
+    "dckv_decode_launch_info": (ctypes.c_int, [_vp, _i32, _i32, ctypes.POINTER(LaunchInfo)]),
     "dckv_latent_append": (ctypes.c_int, [_vp, _vp, _i32, _vp, _vp, _vp, _vp, _i64, _vp]),
     "dckv_decode": (ctypes.c_int, [_vp, _vp, _i32, _vp, _i64, _vp, _i32, _vp, _i32, _vp, _vp, _vp,
                                    _vp, ctypes.c_size_t, _vp]),

@@ -478,6 +478,20 @@ int dckv_decode_workspace_bytes(const dckv_plan* p, int32_t batch, int32_t max_c
   return DCKV_OK;
 }
 
+int dckv_decode_launch_info(const dckv_plan* p, int32_t batch, int32_t max_context,
+                            dckv_launch_info* info) {
+  if (!p || !info) return fail(DCKV_EINVAL, "decode_launch_info: null plan or info pointer");
+  if (batch < 0 || max_context < 0)
+    return fail(DCKV_EINVAL, "decode_launch_info: negative batch %d or max_context %d", batch,
+                max_context);
+  const dckv::DecodeShape sh = dckv::decode_shape(*p, batch, max_context);
+  info->kernels = sh.pass ? 2 : (sh.mfma ? 1 : 0);
+  info->split_tokens = sh.split_tokens;
+  info->n_split = sh.n_split;
+  info->head_slices = sh.mfma ? p->mfma.n_slices : 1;
+  return DCKV_OK;
+}
+
 int dckv_latent_append(const dckv_plan* p, const void* x, int32_t n_tok, const void* L_keys,
                        const void* L_value, const int64_t* slot, void* pool, int64_t num_pages,
                        void* stream) {

@@ -94,6 +94,15 @@ class Plan:
                "decode_workspace_bytes")
         return n.value
 
+    def launch_info(self, batch: int, max_context: int) -> dict:
+        """The launch a decode of `batch` sequences of at most `max_context`
+        tokens takes: kernels (0 portable, 1 single-pass, 2 two-pass),
+        split_tokens, n_split, head_slices."""
+        info = capi.LaunchInfo()
+        _check(_lib.dckv_decode_launch_info(self.handle, batch, max_context, ctypes.byref(info)),
+               "decode_launch_info")
+        return {name: getattr(info, name) for name, _ in capi.LaunchInfo._fields_}
+
     def rope_workspace_bytes(self, batch: int, max_context: int) -> int:
         n = ctypes.c_size_t()
         _check(_lib.dckv_rope_workspace_bytes(self.handle, batch, max_context, ctypes.byref(n)),
