@@ -601,13 +601,15 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
 // Merge: a[b][h][r] = sum_s 2^(m_s - M) acc_s[r] / sum_s 2^(m_s - M) l_s.
 // Grid (batch * slices, value-rank chunks of kMergeRanks), 256 threads.
 // Pass 1: per head slot the maximum M and the weighted sum L over splits,
-// read from the compact (m, l) rows, eight independent loads a thread.
+// read from the compact (m, l) rows, up to 32 (16 pairs) independent loads
+// a thread for long merges, eight for short ones.
 // Pass 2: a split row of the chunk is kMergeRanks * NH contiguous floats;
 // TPR threads cover it with float4 loads (4 head slots each) and the
-// 256 / TPR thread groups take the splits round-robin, four splits in flight.
+// 256 / TPR thread groups take the splits round-robin, sixteen splits in
+// flight for long merges, four for short ones.
 // Fixed order: group g sums splits g, g + G, ... ascending, then the G group
 // sums are added in order.
-template <int NH>
+template <int NH, bool LONG>
 __global__ __launch_bounds__(256) void merge_mfma(const float* __restrict__ part_ml,
                                                   const float* __restrict__ part,
                                                   const int32_t* __restrict__ seq_lens,
@@ -636,6 +638,13 @@ __global__ __launch_bounds__(256) void merge_mfma(const float* __restrict__ part
     const int h = tid % NH, sub = tid / NH;
     float mx = -INFINITY;
     int s = sub;
+    for (; LONG && s + 31 * SUB < ns; s += 32 * SUB) {   // long merges: 32 loads in flight
+      float v[32];
+#pragma unroll
+      for (int k = 0; k < 32; ++k) v[k] = ml[(s + k * SUB) * (2 * NH) + h];
+#pragma unroll
+      for (int k = 0; k < 32; ++k) mx = fmaxf(mx, v[k]);
+    }
     for (; s + 7 * SUB < ns; s += 8 * SUB) {
       float v[8];
 #pragma unroll
@@ -656,6 +665,16 @@ __global__ __launch_bounds__(256) void merge_mfma(const float* __restrict__ part
     float l = 0.f;
     if (M != -INFINITY) {
       s = sub;
+      for (; LONG && s + 15 * SUB < ns; s += 16 * SUB) {   // long merges: 16 pairs in flight
+        float mv[16], lv[16];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          mv[k] = ml[(s + k * SUB) * (2 * NH) + h];
+          lv[k] = ml[(s + k * SUB) * (2 * NH) + NH + h];
+        }
+#pragma unroll
+        for (int k = 0; k < 16; ++k) l += exp2f(mv[k] - M) * lv[k];
+      }
       for (; s + 7 * SUB < ns; s += 8 * SUB) {
         float mv[8], lv[8];
 #pragma unroll
@@ -689,6 +708,21 @@ __global__ __launch_bounds__(256) void merge_mfma(const float* __restrict__ part
     const float* src = pb + int64_t(r) * NH + hq;
     const int64_t stride = int64_t(NH) * rv;
     int s = g;
+    for (; LONG && s + 15 * G < ns; s += 16 * G) {   // long merges: 16 splits in flight
+      float4 mv[16], av[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        mv[k] = *reinterpret_cast<const float4*>(ml + (s + k * G) * (2 * NH) + hq);
+        av[k] = *reinterpret_cast<const float4*>(src + (s + k * G) * stride);
+      }
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        a.x = fmaf(exp2f(mv[k].x - M4.x), av[k].x, a.x);
+        a.y = fmaf(exp2f(mv[k].y - M4.y), av[k].y, a.y);
+        a.z = fmaf(exp2f(mv[k].z - M4.z), av[k].z, a.z);
+        a.w = fmaf(exp2f(mv[k].w - M4.w), av[k].w, a.w);
+      }
+    }
     for (; s + 3 * G < ns; s += 4 * G) {
       float4 mv[4], av[4];
 #pragma unroll
@@ -838,14 +872,14 @@ hipError_t launch_split_pw(const dckv_plan& p, const DecodeShape& sh, const void
 hipError_t launch_merge_upproj(const dckv_plan& p, const DecodeShape& sh, const int32_t* seq_lens,
                                const float* part_ml, const float* part, float* amerged,
                                const void* R_value, float* out, hipStream_t stream) {
-  if (p.mfma.nt == 1)
-    hipLaunchKernelGGL(merge_mfma<16>, dim3(sh.batch * p.mfma.n_slices, sh.n_rchunks), dim3(256), 0,
-                       stream, part_ml, part, seq_lens, sh.max_context, sh.split_tokens,
-                       sh.n_split, p.rv, amerged, p.tables, p.mfma);
-  else
-    hipLaunchKernelGGL(merge_mfma<32>, dim3(sh.batch * p.mfma.n_slices, sh.n_rchunks), dim3(256), 0,
-                       stream, part_ml, part, seq_lens, sh.max_context, sh.split_tokens,
-                       sh.n_split, p.rv, amerged, p.tables, p.mfma);
+  // the deep-batch merge only for long split lists: its registers would cost
+  // the short merges (many small work-groups) their occupancy
+  const bool lng = sh.n_split >= 128;
+  auto kern = p.mfma.nt == 1 ? (lng ? merge_mfma<16, true> : merge_mfma<16, false>)
+                             : (lng ? merge_mfma<32, true> : merge_mfma<32, false>);
+  hipLaunchKernelGGL(kern, dim3(sh.batch * p.mfma.n_slices, sh.n_rchunks), dim3(256), 0, stream,
+                     part_ml, part, seq_lens, sh.max_context, sh.split_tokens, sh.n_split, p.rv,
+                     amerged, p.tables, p.mfma);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_upproj(p, sh.batch * p.Q, amerged, R_value, out, stream);
