@@ -602,10 +602,16 @@ def bench_compressed(args, torch, wl, copy):
               f"decode_waves={plan.geometry['decode_waves']}")
     if Q > 1:
         launch += f" queries_per_seq={Q}"
+    # the two-pass value kernel: waves over pages for one row slice, all
+    # waves over each page for several (the slices sharing one walk)
+    vkern = "value_shared" if info["head_slices"] > 1 else "value_pages"
     if two_pass:
-        launch = f"two_pass chunk_tokens={split_used}"
+        launch = (f"two_pass chunk_tokens={split_used} head_slices={info['head_slices']} "
+                  f"value_tiles={info['value_tiles']}")
+        if Q > 1:
+            launch += f" queries_per_seq={Q}"
     kernel_bytes = nb["value_latent"] if two_pass else nb["latent"]
-    traffic = measured_traffic(wl, launch, Q, "value_pages" if two_pass else "split_mfma") if mfma else None
+    traffic = measured_traffic(wl, launch, Q, vkern if two_pass else "split_mfma") if mfma else None
     achieved = kernel_bytes / (kern_ms * 1e-3) / 1e9
     value = wl.batch * Q / (ms_step * 1e-3)
     decode_gbs = nb["decode_total"] / (ms_decode * 1e-3) / 1e9
@@ -647,7 +653,7 @@ def bench_compressed(args, torch, wl, copy):
         },
         "copy_peak": copy,
         "roofline": {
-            "kernel": ("value pass of the two-pass decode (value_pages)" if two_pass else
+            "kernel": (f"value pass of the two-pass decode ({vkern})" if two_pass else
                        "split-K latent attention (" + ("split_mfma" if mfma else "split_valu") + ")"),
             "bound": "hbm",
             "achieved": achieved,

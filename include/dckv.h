@@ -191,7 +191,11 @@ typedef struct dckv_launch_info {
                             2 two-pass MFMA kernels */
   int32_t split_tokens;  /* context tokens a split (a value chunk on the two-pass path) */
   int32_t n_split;       /* splits (chunks) of the longest sequence */
-  int32_t head_slices;   /* row slices of the single-pass kernel (1 otherwise) */
+  int32_t head_slices;   /* row slices of the MFMA kernels (each slice's score work
+                            reads its groups' key chunks; on the single-pass kernel
+                            each also reads the value part), 1 on the portable path */
+  int32_t value_tiles;   /* two-pass path: 16-rank value tiles a value work-group
+                            (0 otherwise) */
 } dckv_launch_info;
 int dckv_decode_launch_info(const dckv_plan* plan, int32_t batch, int32_t max_context,
                             dckv_launch_info* info);

@@ -81,6 +81,7 @@ class LaunchInfo(ctypes.Structure):
         ("split_tokens", ctypes.c_int32),
         ("n_split", ctypes.c_int32),
         ("head_slices", ctypes.c_int32),
+        ("value_tiles", ctypes.c_int32),
     ]
 
 

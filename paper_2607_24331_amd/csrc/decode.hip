@@ -7,6 +7,7 @@
 //   merge  fixed ascending-split log-sum-exp merge, then o_h = (acc / l)
 //          R_v[:, kv(h) block] (one up-projection per head)
 #include <algorithm>
+#include <vector>
 #include <cmath>
 
 #include "device.h"
@@ -216,12 +217,17 @@ hipError_t launch_decode_t(const dckv_plan& p, const DecodeShape& sh, const floa
 
 // Two-pass shape.  Score work-groups of eight pages, so that ragged batches
 // balance over the compute units.  Value work-groups (sequence, chunk, rank
-// group): the tiles a group (4, 6 or 8) and the chunk count are chosen so
-// that the work-groups fill whole rounds of the compute units -- the
-// estimate is rounds x (pages a wave x (tiles + head tiles, the weight
-// loads counted at half a tile each) + a fixed cost of 4) -- with fewer
-// chunks (fewer partials) on ties; split_tokens / 64, when given, is the
-// chunk length.
+// group): the tiles a group and the chunk count are chosen so that the
+// work-groups fill whole rounds of the compute units, with fewer chunks
+// (fewer partials) on ties; split_tokens / 64, when given, is the chunk
+// length.  One row slice: waves take pages of the chunk, a group of 4, 6 or
+// 8 tiles; the estimate is rounds x (pages a wave x (tiles + head tiles, the
+// weight loads counted at half a tile each) + a fixed cost of 4).  Several
+// slices: the eight waves walk the chunk's pages together, 1, 2 or 4 tiles a
+// wave (4 only for at most 4 row tiles, 1 and 2 for at most 8, 1 beyond);
+// the estimate, in sixteenths of a page of one tile a wave, is rounds x
+// (pages x (16 tiles + 8 + row tiles) + 64): a page's weights staged and a
+// barrier cost about half a tile, each row tile a sixteenth more.
 static DecodeShape pass_shape(const dckv_plan& p, int32_t batch, int32_t max_context) {
   DecodeShape s{};
   s.batch = batch;
@@ -231,15 +237,24 @@ static DecodeShape pass_shape(const dckv_plan& p, int32_t batch, int32_t max_con
   s.npm = int32_t(npm);
   s.unit_pages = 8;
   s.units_per_seq = int32_t((npm + s.unit_pages - 1) / s.unit_pages);
-  const int64_t cap = pass_max_chunk_pages();
+  const int64_t cap = pass_max_chunk_pages(p);
   const int64_t B = std::max<int32_t>(batch, 1);
+  const int32_t RT = p.pass.n_slices * p.pass.nt;
+  const bool shared = p.pass.n_slices > 1;
+  std::vector<int32_t> options;
+  if (!shared) options = {8, 6, 4};
+  else if (RT <= 4) options = {4, 2};
+  else if (RT <= 8) options = {2, 1};
+  else options = {1};
   int64_t best_cost = -1;
-  for (int32_t rgt : {8, 6, 4}) {
-    const int64_t nrg = (p.pass.mt_v + rgt - 1) / rgt;
+  for (int32_t rgt : options) {
+    const int64_t tiles = shared ? 8 * int64_t(rgt) : rgt;   // value tiles a work-group
+    const int64_t nrg = (p.pass.mt_v + tiles - 1) / tiles;
     auto consider = [&](int64_t cp) {
       const int64_t nc = (npm + cp - 1) / cp;
       const int64_t rounds = (B * nc * nrg + kTargetWorkgroups - 1) / kTargetWorkgroups;
-      const int64_t cost = rounds * ((cp + 7) / 8 * (rgt + p.pass.nt) + 4);
+      const int64_t cost = shared ? rounds * (cp * (16 * rgt + 8 + RT) + 64)
+                                  : rounds * ((cp + 7) / 8 * (rgt + p.pass.nt) + 4);
       if (best_cost < 0 || cost < best_cost || (cost == best_cost && nc < s.n_chunks)) {
         best_cost = cost;
         s.rgt = rgt;
@@ -251,22 +266,24 @@ static DecodeShape pass_shape(const dckv_plan& p, int32_t batch, int32_t max_con
     if (p.split_tokens > 0) {
       consider(std::min<int64_t>(cap, std::max<int64_t>(1, p.split_tokens / DCKV_PAGE_TOKENS)));
     } else {
-      for (int64_t nc = (npm + cap - 1) / cap; nc <= std::max<int64_t>(1, 2 * kTargetWorkgroups / (B * nrg)) + 1
-                                               && nc <= npm; ++nc)
-        consider((npm + nc - 1) / nc);
+      // from the fewest chunks the cap allows to about two work-groups a
+      // compute unit (at least the first candidate)
+      const int64_t lo = (npm + cap - 1) / cap;
+      const int64_t hi = std::min(npm, std::max(lo, std::max<int64_t>(1, 2 * kTargetWorkgroups / (B * nrg)) + 1));
+      for (int64_t nc = lo; nc <= hi; ++nc) consider((npm + nc - 1) / nc);
     }
   }
   s.split_tokens = s.chunk_pages * DCKV_PAGE_TOKENS;
   s.n_split = s.n_chunks;
-  const size_t nh = 16 * size_t(p.pass.nt);
+  const size_t ns = 16 * size_t(RT);          // row slots
   s.off_qt = 0;
-  s.off_p = align_up(size_t(batch) * p.pass.max_pairs * 2048, 256);
-  s.off_el = s.off_p + align_up(size_t(batch) * npm * nh * 64 * 2, 256);
-  s.off_ml = s.off_el + align_up(size_t(batch) * npm * p.pass.nt * 512, 256);
+  s.off_p = align_up(size_t(batch) * p.pass.n_slices * p.pass.max_pairs * 2048, 256);
+  s.off_el = s.off_p + align_up(size_t(batch) * npm * ns * 64 * 2, 256);
+  s.off_ml = s.off_el + align_up(size_t(batch) * npm * RT * 512, 256);
   const size_t rows = size_t(batch) * s.n_chunks;
-  s.off_acc = s.off_ml + align_up(rows * 2 * nh * sizeof(float), 256);
-  s.off_opart = s.off_acc + align_up(rows * nh * size_t(p.rv) * sizeof(float), 256);
-  s.bytes = s.off_opart + align_up(size_t(batch) * p.Hq * p.rv * sizeof(float), 256);
+  s.off_acc = s.off_ml + align_up(rows * 2 * ns * sizeof(float), 256);
+  s.off_opart = s.off_acc + align_up(rows * ns * size_t(p.rv) * sizeof(float), 256);
+  s.bytes = s.off_opart + align_up(size_t(batch) * p.Q * p.Hq * p.rv * sizeof(float), 256);
   return s;
 }
 

@@ -41,6 +41,7 @@ constexpr int kRsrcWord3 = 0x00020000;
 constexpr int kOutOfRange = 0x40000000;   // byte offset beyond any page
 constexpr int kNonTemporal = 2;           // cache policy of streamed latents: nt
 constexpr int kMaxChunkPages = 512;       // pages of a value chunk: 64 a wave
+constexpr int kMaxSharedChunkPages = 64;  // pages of a chunk walked by all waves together
 constexpr int kScoreMinLds = 82 * 1024;   // one score work-group a compute unit
 constexpr int kQblkLoads = 20;            // folded-query loads a thread: 80 blocks (the LDS limit)
 
@@ -103,12 +104,17 @@ __device__ __forceinline__ u32x4 scale8(u32x4 v, float f) {
 // its own integer exponent e = ceil(max over its 16 tokens), so no wave waits
 // for another.
 //
-// Outputs per (sequence b, page pg of it, head tile n):
+// With several queries a sequence the rows are cut into J slices (as for
+// the single-pass kernel): work-group (unit, slice) loads the key chunks of
+// its slice's groups, and a row of query i sees positions before
+// T_b - Q + i + 1.
+//
+// Outputs per (sequence b, page pg of it, row tile t = slice * NT + n):
 //   pbuf   2 KB: the weights as the value MFMA's B operand, 16 heads x 64
 //          tokens: k-step ks (tokens 32ks..32ks+31) at ks * 1024 bytes, lane
 //          L = 16 * (t%32 / 8) + head at L * 16, 8 tokens a lane
-//   elbuf  512 B: (e, l) of head j and row block m at floats 8j + 2m and
-//          8j + 2m + 1, l the sum of the block's rounded weights
+//   elbuf  512 B: e and l of row slot j and row block m at floats 8j + m and
+//          8j + 4 + m, l the sum of the block's rounded weights
 template <int NT, int RING>
 __global__ __launch_bounds__(512, 1) void score_pages(
     const u32x4* __restrict__ qblk_ws, const bf16* __restrict__ pool, int64_t num_pages,
@@ -117,9 +123,15 @@ __global__ __launch_bounds__(512, 1) void score_pages(
     int64_t page_elems, uint32_t* __restrict__ pbuf, float* __restrict__ elbuf, MfmaTables mt) {
   constexpr int PP = 2 / NT;                   // pages side by side
   extern __shared__ __align__(16) unsigned char smem[];
-  const int u = blockIdx.x;
+  // the J slices of a page range run side by side on one XCD (block ids
+  // equal mod 8), so a key chunk two slices load comes the second time from
+  // that XCD's L2
+  const int J = mt.n_slices;
+  const int qd = blockIdx.x >> 3, slice = qd % J;
+  const int u = 8 * (qd / J) + (blockIdx.x & 7);
   if (u >= n_units) return;
   const int b = u / units_per_seq, ur = u - b * units_per_seq;
+  const int RT = J * NT;                       // row tiles of a page's outputs
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 15, lq = lane >> 4;
@@ -133,18 +145,20 @@ __global__ __launch_bounds__(512, 1) void score_pages(
   // back.
   const int p0 = ur * unit_pages;
   const int pt = page_table[int64_t(b) * max_pages + min(p0 + pl + PP * lane, max_pages - 1)];
-  const int nch0 = mt.kln[0][0][0] + mt.kln[0][0][1];
-  const int npairs = nch0 + (NT > 1 ? mt.kln[0][1][0] + mt.kln[0][1][1] : 0);
+  const int nch0 = mt.kln[slice][0][0] + mt.kln[slice][0][1];
+  const int npairs = nch0 + (NT > 1 ? mt.kln[slice][1][0] + mt.kln[slice][1][1] : 0);
   u32x4* qblk = reinterpret_cast<u32x4*>(smem);                // [npairs][2][64]
-  const u32x4* qsrc = qblk_ws + int64_t(b) * mt.max_pairs * 128;
+  const u32x4* qsrc = qblk_ws + (int64_t(b) * J + slice) * mt.max_pairs * 128;
   const int n16 = npairs * 128;
   u32x4 qv[kQblkLoads];
 #pragma unroll
   for (int k = 0; k < kQblkLoads; ++k) qv[k] = qsrc[min(tid + 512 * k, n16 - 1)];
   int T_b = seq_lens[b];
 
-  const int st0 = mt.kst[0][n][0], ln0 = mt.kln[0][n][0], st1 = mt.kst[0][n][1];
-  const int nch = ln0 + mt.kln[0][n][1];       // key chunks of this wave's tile
+  const int st0 = mt.kst[slice][n][0], ln0 = mt.kln[slice][n][0], st1 = mt.kst[slice][n][1];
+  const int nch = ln0 + mt.kln[slice][n][1];   // key chunks of this wave's tile
+  // this lane's row (query i, head h) sees positions before T_b - Q + i + 1
+  const int hrow = mt.hord[slice][16 * n + lr];
   const int pair0 = n ? nch0 : 0;
   // lane i: the physical page of this wave's i-th page (-1: invalid)
   const int pid_tbl = (pt >= 0 && pt < num_pages) ? pt : -1;
@@ -154,6 +168,7 @@ __global__ __launch_bounds__(512, 1) void score_pages(
   const int p1 = min(np, p0 + unit_pages);
   const int nmine = max(0, (p1 - p0 - pl + PP - 1) / PP);       // this wave's pages (<= 64)
   const int total = nmine * nch;
+  const int lim = hrow < 0 ? 0 : T_b - mt.queries + hrow / mt.q_heads + 1;
 
   const int page_bytes = int(page_elems * 2);
   const int lane_key = 2 * (lr * 32 + 8 * lq) + 2 * 512 * m;
@@ -203,13 +218,12 @@ __global__ __launch_bounds__(512, 1) void score_pages(
   // the weights of this wave's 16 tokens of page k, from S
   auto epilogue = [&](int k) {
     const int pg = p0 + pl + PP * k;
-    const int nval = min(64, T_b - 64 * pg);
     const bool pvalid = __builtin_amdgcn_readlane(pid_tbl, min(k, 63)) >= 0;
     float mx = -INFINITY;
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      const int tok = 16 * m + 4 * lq + v;
-      if (!pvalid || tok >= nval) S[v] = -INFINITY;
+      const int t = 64 * pg + 16 * m + 4 * lq + v;     // position; t < lim <= T_b
+      if (!pvalid || t >= lim) S[v] = -INFINITY;
       mx = fmaxf(mx, S[v]);
     }
     mx = wave_max16(mx);
@@ -230,13 +244,15 @@ __global__ __launch_bounds__(512, 1) void score_pages(
       pk[v2] = word;
     }
     // tokens 16m + 4lq .. +3: k-step m/2, operand lane 16 * (2(m%2) + lq/2) + lr
-    uint32_t* blk = pbuf + ((int64_t(b) * npm + pg) * NT + n) * 512;
+    const int64_t tile = (int64_t(b) * npm + pg) * RT + slice * NT + n;
+    uint32_t* blk = pbuf + tile * 512;
     const int L = 16 * (2 * (m & 1) + (lq >> 1)) + lr;
     *reinterpret_cast<uint2*>(blk + (m >> 1) * 256 + L * 4 + 2 * (lq & 1)) = uint2{pk[0], pk[1]};
     psum = wave_sum16(psum);
-    if (lq == 0)
-      *reinterpret_cast<float2*>(elbuf + ((int64_t(b) * npm + pg) * NT + n) * 128 + 8 * lr + 2 * m) =
-          make_float2(e, psum);
+    if (lq == 0) {
+      elbuf[tile * 128 + 8 * lr + m] = e;
+      elbuf[tile * 128 + 8 * lr + 4 + m] = psum;
+    }
     S = floatx4{0.f, 0.f, 0.f, 0.f};
   };
 
@@ -375,14 +391,14 @@ __global__ __launch_bounds__(W * 64, 1) void value_pages(
       float fa[NT];
 #pragma unroll
       for (int n = 0; n < NT; ++n) {
-        const float4 ea = __builtin_bit_cast(float4, ring[2 * n]);       // (e0, l0, e1, l1)
-        const float4 eb = __builtin_bit_cast(float4, ring[2 * n + 1]);   // (e2, l2, e3, l3)
-        const float em = fmaxf(fmaxf(ea.x, ea.z), fmaxf(eb.x, eb.z));
+        const float4 ev = __builtin_bit_cast(float4, ring[2 * n]);       // (e0, e1, e2, e3)
+        const float4 lv = __builtin_bit_cast(float4, ring[2 * n + 1]);   // (l0, l1, l2, l3)
+        const float em = fmaxf(fmaxf(ev.x, ev.y), fmaxf(ev.z, ev.w));
         const float En = fmaxf(E_run[n], em);
         fa[n] = E_run[n] == -INFINITY ? 1.f : pow2_rel(E_run[n], En);
-        const float f0 = pow2_rel(ea.x, En), f1 = pow2_rel(ea.z, En);
-        const float f2 = pow2_rel(eb.x, En), f3 = pow2_rel(eb.z, En);
-        L_run[n] = L_run[n] * fa[n] + (((ea.y * f0 + ea.w * f1) + eb.y * f2) + eb.w * f3);
+        const float f0 = pow2_rel(ev.x, En), f1 = pow2_rel(ev.y, En);
+        const float f2 = pow2_rel(ev.z, En), f3 = pow2_rel(ev.w, En);
+        L_run[n] = L_run[n] * fa[n] + (((lv.x * f0 + lv.y * f1) + lv.z * f2) + lv.w * f3);
         E_run[n] = En;
         // lane quarter lq holds tokens 32 ks + 8 lq ..: row block 2 ks + lq / 2
         fks[n][0] = (lq >> 1) ? f1 : f0;
@@ -466,19 +482,233 @@ __global__ __launch_bounds__(W * 64, 1) void value_pages(
 }
 
 // ---------------------------------------------------------------------------
-// Merge of the chunks: a[b][h][r] = sum_c 2^(E_c - M) acc_c[r] / sum_c
+// Value pass for several row slices (several queries a sequence).  Work-group
+// (sequence b, chunk c, rank group g): the eight waves walk the chunk's pages
+// together, wave w owning value tiles g * 8 * RGTW + w * RGTW .. + RGTW - 1
+// against all RT row tiles, so each value latent byte is read once.  The
+// weights of a page are staged in LDS already rescaled to the running
+// exponents: thread i of the staging holds weight operand element i (row
+// tile t, k-step, operand lane) of every page and keeps the running exponent
+// E of that element's row slot (the same in every thread holding that slot:
+// the same records in the same order), and the holder of k-step 0, lanes
+// 0..15 also keeps the slot's running sum L and stages the factor 2^(E_old -
+// E_new) by which the waves rescale their accumulators.  Two buffers, one
+// barrier a page: the next page's weights load while the current one is
+// used; a wave's value loads run DP pages ahead.
+// Partials as value_pages, over NS = 16 RT row slots; no sums across waves.
+template <int RTMAX, int RGTW, int DP>
+__global__ __launch_bounds__(512, 1) void value_shared(
+    const bf16* __restrict__ pool, int64_t num_pages, const int32_t* __restrict__ page_table,
+    int max_pages, const int32_t* __restrict__ seq_lens, int max_context, int chunk_pages,
+    int n_chunks, int n_rg, int batch, int npm, int rv, int mt_v, int64_t page_elems,
+    int64_t value_base, int RT, const u32x4* __restrict__ pbuf, const u32x4* __restrict__ elbuf,
+    float* __restrict__ vpart, float* __restrict__ vel) {
+  constexpr int W = 8;
+  constexpr int IP = 2 * RGTW;                      // value loads a page a wave
+  constexpr int RING = DP * IP;
+  constexpr int SV = (RTMAX * 128 + 511) / 512;     // weight elements a staging thread
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int Lb = blockIdx.x;
+  const int xcd = Lb & 7, qd = Lb >> 3;
+  const int rg = qd % n_rg;
+  const int cidx = 8 * (qd / n_rg) + xcd;          // sequence * n_chunks + chunk
+  if (cidx >= batch * n_chunks) return;
+  const int b = cidx / n_chunks, chunk = cidx - b * n_chunks;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lr = lane & 15, lq = lane >> 4;
+  const int NS = 16 * RT;
+
+  // lane i: the physical page of the chunk's i-th page (chunk_pages <= 64)
+  const int g0 = chunk * chunk_pages;               // < npm
+  const int pt = page_table[int64_t(b) * max_pages + min(g0 + lane, max_pages - 1)];
+  int T_b = seq_lens[b];
+  T_b = T_b < 0 ? 0 : (T_b > max_context ? max_context : T_b);
+  const int np = (T_b + 63) >> 6;
+  const int npg = max(0, min(np, g0 + chunk_pages) - g0);   // the chunk's pages
+  const int pid_tbl = (pt >= 0 && pt < num_pages) ? pt : -1;
+  const int mt0 = rg * W * RGTW + w * RGTW;          // this wave's first value tile
+
+  // LDS, two buffers: weights [RT][2][64] u32x4, then factors [NS] floats
+  const int nw = RT * 128;
+  u32x4* wbuf = reinterpret_cast<u32x4*>(smem);
+  float* fbuf = reinterpret_cast<float*>(wbuf + 2 * nw);
+  const u32x4* pb0 = pbuf + int64_t(b) * npm * RT * 128;
+  const u32x4* eb0 = elbuf + int64_t(b) * npm * RT * 32;
+  u32x4 sw[SV], se[SV], sl[SV];                     // raw weights, e and l records of the slot
+  float Er[SV], Lr[SV];
+#pragma unroll
+  for (int k = 0; k < SV; ++k) {
+    Er[k] = -INFINITY;
+    Lr[k] = 0.f;
+  }
+  auto stage_load = [&](int pg) {                   // pg < npm: loads at clamped indices
+#pragma unroll
+    for (int k = 0; k < SV; ++k) {
+      const int i = min(tid + 512 * k, nw - 1);
+      const int slot = 16 * (i >> 7) + (i & 15);
+      sw[k] = pb0[int64_t(pg) * RT * 128 + i];
+      se[k] = eb0[int64_t(pg) * RT * 32 + 2 * slot];
+      sl[k] = eb0[int64_t(pg) * RT * 32 + 2 * slot + 1];
+    }
+  };
+  auto stage_store = [&](int buf) {
+#pragma unroll
+    for (int k = 0; k < SV; ++k) {
+      const int i = tid + 512 * k;
+      if (i < nw) {
+        const float4 ev = __builtin_bit_cast(float4, se[k]);
+        const float En = fmaxf(Er[k], fmaxf(fmaxf(ev.x, ev.y), fmaxf(ev.z, ev.w)));
+        const float f0 = pow2_rel(ev.x, En), f1 = pow2_rel(ev.y, En);
+        const float f2 = pow2_rel(ev.z, En), f3 = pow2_rel(ev.w, En);
+        // operand lane L holds tokens 32 ks + 8 (L / 16) ..: row block 2 ks + L / 32
+        const int ks = (i >> 6) & 1, hi = (i >> 5) & 1;
+        const float f = ks ? (hi ? f3 : f2) : (hi ? f1 : f0);
+        wbuf[buf * nw + i] = scale8(sw[k], f);
+        if ((i & 127) < 16) {                       // k-step 0, lanes 0..15: slot 16 t + i % 16
+          const float4 lv = __builtin_bit_cast(float4, sl[k]);
+          const float fa = Er[k] == -INFINITY ? 1.f : pow2_rel(Er[k], En);
+          Lr[k] = Lr[k] * fa + (((lv.x * f0 + lv.y * f1) + lv.z * f2) + lv.w * f3);
+          fbuf[buf * NS + 16 * (i >> 7) + (i & 15)] = fa;
+        }
+        Er[k] = En;
+      }
+    }
+  };
+
+  const int page_bytes = int(page_elems * 2);
+  const int lane_val = 2 * (lr * 32 + 8 * lq);
+  __amdgpu_buffer_rsrc_t rsrc;
+  int pnval = 0;
+  auto set_page = [&](int k) {                      // value loads of the chunk's page k
+    const int pid = __builtin_amdgcn_readlane(pid_tbl, min(k, 63));
+    const bool ok = k < npg && pid >= 0;
+    pnval = k < npg ? min(64, T_b - 64 * (g0 + k)) : 0;
+    rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<bf16*>(ok ? pool + int64_t(pid) * page_elems : pool), 0, ok ? page_bytes : 0,
+        kRsrcWord3);
+  };
+  auto issue = [&](int s) -> u32x4 {                // item s: value tile s / 2, k-step s % 2
+    const int i = s >> 1, ks = s & 1;
+    const int o = 2 * (int(value_base) + 1024 * (mt0 + i) + 512 * ks) + lane_val;
+    const bool ok = (mt0 + i < mt_v) & (16 * (mt0 + i) + lr < rv) & (32 * ks + 8 * lq < pnval);
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                         rsrc, ok ? o : kOutOfRange, 0, kNonTemporal));
+  };
+
+  u32x4 ring[RING];
+  stage_load(g0);
+#pragma unroll
+  for (int d = 0; d < DP; ++d) {
+    set_page(d);
+#pragma unroll
+    for (int s = 0; s < IP; ++s) ring[d * IP + s] = issue(s);
+  }
+  if (npg > 0) stage_store(0);
+  __syncthreads();
+
+  floatx4 acc[RGTW][RTMAX];
+#pragma unroll
+  for (int i = 0; i < RGTW; ++i)
+#pragma unroll
+    for (int t = 0; t < RTMAX; ++t) acc[i][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  // page k of the chunk, its value loads in ring slots d * IP ..
+  auto page = [&](int k, int d) {
+    const int cur = k & 1;
+    const bool more = k + 1 < npg;
+    stage_load(g0 + (more ? k + 1 : k));            // the next page's weights, in flight
+    const u32x4* lb = wbuf + cur * nw;
+    float fa[RTMAX];
+    bool resc = false;
+#pragma unroll
+    for (int t = 0; t < RTMAX; ++t) {
+      fa[t] = t < RT ? fbuf[cur * NS + 16 * t + lr] : 1.f;
+      resc = resc || fa[t] != 1.f;
+    }
+    if (__any(resc)) {
+#pragma unroll
+      for (int i = 0; i < RGTW; ++i)
+#pragma unroll
+        for (int t = 0; t < RTMAX; ++t) acc[i][t] *= fa[t];
+    }
+    const int nval = min(64, T_b - 64 * (g0 + k));
+    const int keep0 = min(8, max(0, nval - 8 * lq));
+    const int keep1 = min(8, max(0, nval - 32 - 8 * lq));
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      u32x4 a[RGTW];
+#pragma unroll
+      for (int i = 0; i < RGTW; ++i) {
+        a[i] = ring[d * IP + 2 * i + ks];
+        if (nval < 64) a[i] = keep_first(a[i], ks ? keep1 : keep0);
+      }
+#pragma unroll
+      for (int t = 0; t < RTMAX; ++t) {
+        if (t < RT) {
+          const u32x4 B = lb[t * 128 + ks * 64 + lane];
+#pragma unroll
+          for (int i = 0; i < RGTW; ++i) acc[i][t] = mfma(a[i], B, acc[i][t]);
+        }
+      }
+    }
+    set_page(k + DP);                                // refill this page's slots
+#pragma unroll
+    for (int s = 0; s < IP; ++s) ring[d * IP + s] = issue(s);
+    if (more) stage_store(cur ^ 1);
+    __syncthreads();
+  };
+  int k0 = 0;
+  for (; k0 + DP <= npg; k0 += DP) {
+#pragma unroll
+    for (int d = 0; d < DP; ++d) page(k0 + d, d);
+  }
+#pragma unroll
+  for (int d = 0; d < DP; ++d)
+    if (k0 + d < npg) page(k0 + d, d);
+
+  if (npg == 0) return;
+  float* vp = vpart + int64_t(cidx) * NS * rv;
+#pragma unroll
+  for (int i = 0; i < RGTW; ++i) {
+    const int r0 = 16 * (mt0 + i) + 4 * lq;
+#pragma unroll
+    for (int t = 0; t < RTMAX; ++t) {
+      if (t < RT && mt0 + i < mt_v) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          if (r0 + v < rv) vp[int64_t(16 * t + lr) * rv + r0 + v] = acc[i][t][v];
+      }
+    }
+  }
+  if (rg == 0) {
+#pragma unroll
+    for (int k = 0; k < SV; ++k) {
+      const int i = tid + 512 * k;
+      if (i < nw && (i & 127) < 16) {
+        const int slot = 16 * (i >> 7) + (i & 15);
+        vel[int64_t(cidx) * 2 * NS + slot] = Er[k];
+        vel[int64_t(cidx) * 2 * NS + NS + slot] = Lr[k];
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Merge of the chunks: a[b][row][r] = sum_c 2^(E_c - M) acc_c[r] / sum_c
 // 2^(E_c - M) L_c, chunks in ascending order, with the running maximum
-// rescaled by exact powers of two.  Grid (batch * NH head slots, rank blocks
-// of 256).
-template <int NH>
+// rescaled by exact powers of two.  Grid (batch * NS row slots, rank blocks
+// of 256); slot 16 t + j is row hord[t / NT][16 (t % NT) + j] (query i, head
+// h as i * H_q + h).
 __global__ __launch_bounds__(256) void merge_chunks(const float* __restrict__ vpart,
                                                     const float* __restrict__ vel,
                                                     const int32_t* __restrict__ seq_lens,
                                                     int max_context, int chunk_pages, int n_chunks,
-                                                    int rv, float* __restrict__ amerged,
-                                                    int n_q_heads, MfmaTables mt) {
-  const int b = blockIdx.x / NH, j = blockIdx.x % NH;
-  const int row = mt.hord[0][j];
+                                                    int rv, int NS, float* __restrict__ amerged,
+                                                    MfmaTables mt) {
+  const int b = blockIdx.x / NS, j = blockIdx.x % NS;
+  const int nh = 16 * mt.nt;
+  const int row = mt.hord[j / nh][j % nh];
   if (row < 0) return;
   const int r = blockIdx.y * 256 + threadIdx.x;
   if (r >= rv) return;
@@ -486,17 +716,17 @@ __global__ __launch_bounds__(256) void merge_chunks(const float* __restrict__ vp
   T_b = T_b < 0 ? 0 : (T_b > max_context ? max_context : T_b);
   const int np = (T_b + 63) >> 6;
   const int nc = (np + chunk_pages - 1) / chunk_pages;
-  const float* e_b = vel + int64_t(b) * n_chunks * 2 * NH + j;
-  const float* a_b = vpart + (int64_t(b) * n_chunks * NH + j) * rv + r;
+  const float* e_b = vel + int64_t(b) * n_chunks * 2 * NS + j;
+  const float* a_b = vpart + (int64_t(b) * n_chunks * NS + j) * rv + r;
   float M = -INFINITY, a = 0.f, l = 0.f;
   int c = 0;
   for (; c + 8 <= nc; c += 8) {
     float ev[8], lv[8], av[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
-      ev[k] = e_b[(c + k) * 2 * NH];
-      lv[k] = e_b[(c + k) * 2 * NH + NH];
-      av[k] = a_b[int64_t(c + k) * NH * rv];
+      ev[k] = e_b[(c + k) * 2 * NS];
+      lv[k] = e_b[(c + k) * 2 * NS + NS];
+      av[k] = a_b[int64_t(c + k) * NS * rv];
     }
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
@@ -508,15 +738,16 @@ __global__ __launch_bounds__(256) void merge_chunks(const float* __restrict__ vp
     }
   }
   for (; c < nc; ++c) {
-    const float ev = e_b[c * 2 * NH], lv = e_b[c * 2 * NH + NH];
-    const float av = a_b[int64_t(c) * NH * rv];
+    const float ev = e_b[c * 2 * NS], lv = e_b[c * 2 * NS + NS];
+    const float av = a_b[int64_t(c) * NS * rv];
     const float Mn = fmaxf(M, ev);
     const float fo = pow2_rel(M, Mn), fn = pow2_rel(ev, Mn);
     a = a * fo + av * fn;
     l = l * fo + lv * fn;
     M = Mn;
   }
-  amerged[(int64_t(b) * n_q_heads + row) * rv + r] = (M == -INFINITY || !(l > 0.f)) ? 0.f : a / l;
+  amerged[(int64_t(b) * mt.queries * mt.q_heads + row) * rv + r] =
+      (M == -INFINITY || !(l > 0.f)) ? 0.f : a / l;
 }
 
 // ---------------------------------------------------------------------------
@@ -657,6 +888,8 @@ size_t pass_score_lds_bytes(const dckv_plan& p) {
 }
 
 size_t pass_value_lds_bytes(const dckv_plan& p, int rgt) {
+  if (p.pass.n_slices > 1)   // two pages' weights and factors, 2 KB + 64 B a row tile
+    return size_t(2) * p.pass.n_slices * p.pass.nt * (2048 + 64);
   const int nh = 16 * p.pass.nt, W = 8;
   return size_t(2) * W * nh * 4 + size_t(W) * rgt * p.pass.nt * 64 * 16;
 }
@@ -666,7 +899,9 @@ size_t upproj_lds_bytes(const dckv_plan& p, int ct) {
   return std::max<size_t>(size_t(8) * p.rv, size_t(2048 / ct) * (8 * ct + 1)) * 4;
 }
 
-int pass_max_chunk_pages() { return kMaxChunkPages; }
+int pass_max_chunk_pages(const dckv_plan& p) {
+  return p.pass.n_slices > 1 ? kMaxSharedChunkPages : kMaxChunkPages;
+}
 
 template <int NT, int RGT>
 hipError_t launch_value(const dckv_plan& p, const DecodeShape& sh, const void* pool,
@@ -694,6 +929,48 @@ hipError_t launch_value(const dckv_plan& p, const DecodeShape& sh, const void* p
   return hipGetLastError();
 }
 
+template <int RTMAX, int RGTW, int DP>
+hipError_t launch_shared(const dckv_plan& p, const DecodeShape& sh, const void* pool,
+                         int64_t num_pages, const int32_t* page_table, int32_t max_pages,
+                         const int32_t* seq_lens, const u32x4* pbuf, const u32x4* elbuf,
+                         float* vpart, float* vel, hipStream_t stream) {
+  auto kern = value_shared<RTMAX, RGTW, DP>;
+  const size_t lds = pass_value_lds_bytes(p, RGTW);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+  if (e != hipSuccess) return e;
+  const int bc = sh.batch * sh.n_chunks;
+  const dim3 grid(unsigned(8 * sh.n_rgroups * ((bc + 7) / 8)));
+  const int RT = p.pass.n_slices * p.pass.nt;
+  if (p.prof_before && p.prof_after)
+    hipExtLaunchKernelGGL(kern, grid, dim3(512), uint32_t(lds), stream, p.prof_before, p.prof_after,
+                          0u, static_cast<const bf16*>(pool), num_pages, page_table, max_pages,
+                          seq_lens, sh.max_context, sh.chunk_pages, sh.n_chunks, sh.n_rgroups,
+                          sh.batch, sh.npm, p.rv, p.pass.mt_v, p.page_elems, p.value_base, RT, pbuf,
+                          elbuf, vpart, vel);
+  else
+    hipLaunchKernelGGL(kern, grid, dim3(512), lds, stream, static_cast<const bf16*>(pool), num_pages,
+                       page_table, max_pages, seq_lens, sh.max_context, sh.chunk_pages, sh.n_chunks,
+                       sh.n_rgroups, sh.batch, sh.npm, p.rv, p.pass.mt_v, p.page_elems, p.value_base,
+                       RT, pbuf, elbuf, vpart, vel);
+  return hipGetLastError();
+}
+
+// The shared-weights value pass for RT row tiles and RGTW value tiles a wave.
+hipError_t launch_value_shared(const dckv_plan& p, const DecodeShape& sh, const void* pool,
+                               int64_t num_pages, const int32_t* page_table, int32_t max_pages,
+                               const int32_t* seq_lens, const u32x4* pbuf, const u32x4* elbuf,
+                               float* vpart, float* vel, hipStream_t stream) {
+  const int RT = p.pass.n_slices * p.pass.nt;
+#define DCKV_SHARED(RTMAX, RGTW, DP) \
+  launch_shared<RTMAX, RGTW, DP>(p, sh, pool, num_pages, page_table, max_pages, seq_lens, pbuf, elbuf, vpart, vel, stream)
+  if (RT <= 4) return sh.rgt == 4 ? DCKV_SHARED(4, 4, 2) : DCKV_SHARED(4, 2, 4);
+  if (RT <= 8) return sh.rgt == 2 ? DCKV_SHARED(8, 2, 3) : DCKV_SHARED(8, 1, 6);
+#undef DCKV_SHARED
+  return launch_shared<16, 1, 3>(p, sh, pool, num_pages, page_table, max_pages, seq_lens, pbuf,
+                                 elbuf, vpart, vel, stream);
+}
+
 template <int NT, int RING>
 hipError_t launch_score_r(const dckv_plan& p, const DecodeShape& sh, const u32x4* qblk,
                           const void* pool, int64_t num_pages, const int32_t* page_table,
@@ -705,7 +982,7 @@ hipError_t launch_score_r(const dckv_plan& p, const DecodeShape& sh, const u32x4
                                      hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
   if (e != hipSuccess) return e;
   const int n_units = sh.batch * sh.units_per_seq;
-  hipLaunchKernelGGL(kern, dim3(n_units), dim3(512), lds, stream, qblk,
+  hipLaunchKernelGGL(kern, dim3(8 * p.pass.n_slices * ((n_units + 7) / 8)), dim3(512), lds, stream, qblk,
                      static_cast<const bf16*>(pool), num_pages, page_table, max_pages, seq_lens,
                      sh.max_context, sh.unit_pages, sh.units_per_seq, n_units, sh.npm, p.RK,
                      p.page_elems, pbuf, elbuf, p.pass);
@@ -771,22 +1048,22 @@ hipError_t launch_decode_pass(const dckv_plan& p, const DecodeShape& sh, const f
   const u32x4* el4 = reinterpret_cast<const u32x4*>(elbuf);
 #define DCKV_VALUE(NT, RGT) \
   launch_value<NT, RGT>(p, sh, pool, num_pages, page_table, max_pages, seq_lens, pb4, el4, vpart, vel, stream)
-  if (p.pass.nt == 1)
+  if (p.pass.n_slices > 1)
+    e = launch_value_shared(p, sh, pool, num_pages, page_table, max_pages, seq_lens, pb4, el4, vpart,
+                            vel, stream);
+  else if (p.pass.nt == 1)
     e = sh.rgt == 8 ? DCKV_VALUE(1, 8) : sh.rgt == 6 ? DCKV_VALUE(1, 6) : DCKV_VALUE(1, 4);
   else
     e = sh.rgt == 8 ? DCKV_VALUE(2, 8) : sh.rgt == 6 ? DCKV_VALUE(2, 6) : DCKV_VALUE(2, 4);
 #undef DCKV_VALUE
   if (e != hipSuccess) return e;
-  const dim3 mgrid(unsigned(sh.batch * 16 * p.pass.nt), unsigned((p.rv + 255) / 256));
-  if (p.pass.nt == 1)
-    hipLaunchKernelGGL(merge_chunks<16>, mgrid, dim3(256), 0, stream, vpart, vel, seq_lens,
-                       sh.max_context, sh.chunk_pages, sh.n_chunks, p.rv, amerged, p.Hq, p.pass);
-  else
-    hipLaunchKernelGGL(merge_chunks<32>, mgrid, dim3(256), 0, stream, vpart, vel, seq_lens,
-                       sh.max_context, sh.chunk_pages, sh.n_chunks, p.rv, amerged, p.Hq, p.pass);
+  const int NS = 16 * p.pass.nt * p.pass.n_slices;       // row slots
+  hipLaunchKernelGGL(merge_chunks, dim3(unsigned(sh.batch * NS), unsigned((p.rv + 255) / 256)),
+                     dim3(256), 0, stream, vpart, vel, seq_lens, sh.max_context, sh.chunk_pages,
+                     sh.n_chunks, p.rv, NS, amerged, p.pass);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return launch_upproj(p, sh.batch, amerged, R_value, out, stream);
+  return launch_upproj(p, sh.batch * p.Q, amerged, R_value, out, stream);
 }
 
 }  // namespace dckv

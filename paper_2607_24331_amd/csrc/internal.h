@@ -91,8 +91,9 @@ struct DecodeShape {
   int32_t units_per_seq;    // score work-groups a sequence
   int32_t chunk_pages;      // pages a value chunk
   int32_t n_chunks;         // value chunks a sequence
-  int32_t rgt;              // 16-rank value tiles a value work-group: 4, 6 or 8
-  int32_t n_rgroups;        // value rank groups: ceil(r_v / (16 rgt))
+  int32_t rgt;              // 16-rank value tiles a value work-group (4, 6 or 8), or with
+                            // several row slices a wave (1, 2 or 4; eight waves a work-group)
+  int32_t n_rgroups;        // value rank groups: ceil(r_v / (16 rgt)), with slices ceil(r_v / (128 rgt))
   size_t off_qt;            // workspace byte offsets
   size_t off_ml;            // (m, l) of splits; two-pass: (E, L) of chunks
   size_t off_acc;           // split accumulators; two-pass: chunk accumulators
@@ -124,8 +125,8 @@ struct dckv_plan {
   dckv::HeadTables tables;
   bool mfma_ok = false;              // bf16 single-pass MFMA decode path applies
   dckv::MfmaTables mfma{};
-  bool pass_ok = false;              // bf16 two-pass decode applies (one query, <= 32 heads)
-  dckv::MfmaTables pass{};           // its tables: one slice, group order by fewest chunk loads
+  bool pass_ok = false;              // bf16 two-pass decode applies (<= 256 (query, head) rows)
+  dckv::MfmaTables pass{};           // its tables: slices of <= 32 rows, fewest chunk loads
   int32_t pass_ring = 0;             // score-pass loads in flight a wave (16 or 32)
   int32_t key_chunk_loads = 0;       // key chunks the MFMA tiles load a page
   dckv::RopeTables rope{};           // rotary decode tables (valid with mfma_ok)
@@ -162,7 +163,7 @@ void build_pass_tables(dckv_plan& p);
 // Two-pass decode (decode_pass.hip).
 size_t pass_score_lds_bytes(const dckv_plan& p);
 size_t pass_value_lds_bytes(const dckv_plan& p, int rgt);
-int pass_max_chunk_pages();
+int pass_max_chunk_pages(const dckv_plan& p);
 hipError_t launch_decode_pass(const dckv_plan& p, const DecodeShape& sh, const float* q,
                               const void* pool, int64_t num_pages, const int32_t* page_table,
                               int32_t max_pages, const int32_t* seq_lens, const void* R_keys,

@@ -182,27 +182,33 @@ void build_mfma_tables(dckv_plan& p) {
   p.mfma_ok = true;
 }
 
-// Tables of the two-pass decode: one query a sequence and at most 32 query
-// heads, all in one slice of one or two 16-row tiles.  The score pass loads,
-// a page, the key chunks of each tile's groups, so the group order is the
-// one with the fewest chunk loads (every order for up to seven groups, else
-// the group-id order; ties keep the earlier order).  Any value rank: the
-// value pass takes 16-rank tiles in groups of 4, 6 or 8 (chosen per call).
+// Tables of the two-pass decode: the (query, head) rows in J = ceil(rows / 32)
+// slices of one or two 16-row tiles (at most 8 slices), rows of a group
+// together.  The score pass loads, a page, the key chunks of each tile's
+// groups, so the group order is the one with the fewest chunk loads (every
+// order for up to seven groups, else the group-id order; ties keep the
+// earlier order).  Any value rank: the value pass takes 16-rank tiles in
+// groups chosen per call.
 void build_pass_tables(dckv_plan& p) {
   p.pass_ok = false;
   p.pass = MfmaTables{};
   p.pass_ring = 0;
-  if (p.dtype != DCKV_BF16 || p.dh % 8 != 0 || p.Q != 1 || p.Hq > kSliceHeads) return;
+  if (p.dtype != DCKV_BF16 || p.dh % 8 != 0) return;
   if (p.head_slices > 1 || p.decode_waves == 4) return;   // explicit single-pass shapes
+  const int32_t nrows = p.Q * p.Hq;
+  const int32_t J = (nrows + kSliceHeads - 1) / kSliceHeads;
+  if (J > kMaxSlices) return;
+  const int32_t per = (nrows + J - 1) / J;
   MfmaTables& t = p.pass;
-  t.n_slices = 1;
+  t.n_slices = J;
   t.q_heads = p.Hq;
-  t.queries = 1;
-  t.nt = (p.Hq + 15) / 16;
+  t.queries = p.Q;
+  t.nt = (per + 15) / 16;
   t.mt_v = (p.rv + 15) / 16;
   t.waves = 8;
   std::vector<std::vector<int32_t>> rows_of(p.G);
-  for (int32_t h = 0; h < p.Hq; ++h) rows_of[p.group_of_kv[h / p.qpk]].push_back(h);
+  for (int32_t h = 0; h < p.Hq; ++h)
+    for (int32_t i = 0; i < p.Q; ++i) rows_of[p.group_of_kv[h / p.qpk]].push_back(i * p.Hq + h);
   std::vector<int32_t> gorder(p.G);
   for (int32_t g = 0; g < p.G; ++g) gorder[g] = g;
   const bool search = p.G <= 7;
@@ -210,7 +216,7 @@ void build_pass_tables(dckv_plan& p) {
   int32_t best_total = -1;
   do {
     int32_t total = 0;
-    if (!place_rows(p, rows_of, gorder, 1, p.Hq, cand, &total)) continue;
+    if (!place_rows(p, rows_of, gorder, J, per, cand, &total)) continue;
     if (best_total < 0 || total < best_total) {
       best = cand;
       best_total = total;
@@ -419,8 +425,8 @@ int dckv_plan_create(const dckv_layer_desc* d, dckv_plan** out) {
   dckv::build_rope_tables(*p);
   if (p->decode_passes == 2 && !p->pass_ok) {
     delete p;
-    return fail(DCKV_EINVAL, "plan_create: decode_passes 2 needs bf16 latents, one query a sequence, "
-                "at most 32 query heads and d_h a multiple of 8");
+    return fail(DCKV_EINVAL, "plan_create: decode_passes 2 needs bf16 latents, at most 256 (query, "
+                "head) rows, d_h a multiple of 8 and no explicit head_slices or decode_waves 4");
   }
   if (p->decode_passes == 1) p->pass_ok = false;
   *out = p;
@@ -488,7 +494,8 @@ int dckv_decode_launch_info(const dckv_plan* p, int32_t batch, int32_t max_conte
   info->kernels = sh.pass ? 2 : (sh.mfma ? 1 : 0);
   info->split_tokens = sh.split_tokens;
   info->n_split = sh.n_split;
-  info->head_slices = sh.mfma ? p->mfma.n_slices : 1;
+  info->head_slices = sh.pass ? p->pass.n_slices : (sh.mfma ? p->mfma.n_slices : 1);
+  info->value_tiles = sh.pass ? (p->pass.n_slices > 1 ? 8 * sh.rgt : sh.rgt) : 0;
   return DCKV_OK;
 }
 

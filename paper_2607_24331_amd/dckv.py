@@ -97,7 +97,7 @@ class Plan:
     def launch_info(self, batch: int, max_context: int) -> dict:
         """The launch a decode of `batch` sequences of at most `max_context`
         tokens takes: kernels (0 portable, 1 single-pass, 2 two-pass),
-        split_tokens, n_split, head_slices."""
+        split_tokens, n_split, head_slices, value_tiles."""
         info = capi.LaunchInfo()
         _check(_lib.dckv_decode_launch_info(self.handle, batch, max_context, ctypes.byref(info)),
                "decode_launch_info")

@@ -388,19 +388,25 @@ def every_sequence_pairs(wl):
     return pairs
 
 
-def test_multi_query_long_layer_benchmarked_shape():
+@pytest.mark.parametrize("passes", [1, 0])
+def test_multi_query_long_layer_benchmarked_shape(passes):
     # the long-context layer with 4 causal queries a sequence, in the launch
-    # shape the benchmark times (4 row slices, 2048-token splits); rows of
-    # two heads (different groups) for every query, query 0 included
+    # shapes the benchmark times: the single-pass kernel (4 row slices,
+    # 2048-token splits), and the default, the two-pass kernels (the 4 slices
+    # sharing one walk over the value latents); rows of two heads (different
+    # groups) for every query, query 0 included
     from paper_2607_24331_amd import Plan, decode
     wl = make_workload("mha_long_t128k")
-    print("[parity] start mha_long_t128k Q=4", flush=True)
+    print(f"[parity] start mha_long_t128k Q=4 passes {passes}", flush=True)
     inp = make_inputs(wl)
     Q = 4
     plan = Plan(wl.hidden, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_of_kv,
-                wl.group_rank, wl.value_rank, wl.dtype, 2048, queries_per_seq=Q)
+                wl.group_rank, wl.value_rank, wl.dtype, 2048 if passes == 1 else 0,
+                queries_per_seq=Q, decode_passes=passes)
     geo = plan.geometry
-    assert geo["mfma_path"] == 1 and geo["head_slices"] == 4 and geo["two_pass"] == 0
+    assert geo["mfma_path"] == 1 and geo["head_slices"] == 4
+    info = plan.launch_info(wl.batch, int(max(wl.seq_lens)))
+    assert info["kernels"] == (1 if passes == 1 else 2) and info["head_slices"] == 4, info
     pool = gpu_pool_with_append(inp, plan)
     qm = np.random.default_rng(12).standard_normal(
         (wl.batch, Q, wl.num_q_heads, wl.head_dim)).astype(np.float32)
@@ -423,7 +429,7 @@ def test_multi_query_long_layer_benchmarked_shape():
             ref = oattn.attend(qm[0, i, h], K[:n], V[:n])
             errs.append(row_rel_err(got[0, i, h], ref))
         del K, V
-    _report("mha_long_t128k/Q4", errs)
+    _report(f"mha_long_t128k/Q4/{'single' if passes == 1 else 'two'}-pass", errs)
     assert max(errs) <= TOL_REL_ROW
 
 

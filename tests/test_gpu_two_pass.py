@@ -2,14 +2,18 @@
 softmax weights with an integer exponent, value pass over value-rank groups,
 chunk merge, up-projection) against the CPU oracle, on every output row of
 small layers spanning ragged tails, empty and one-token sequences, singleton
-groups, odd ranks, GQA, permuted pages, value ranks above 2048, and softmax
-weights spread over hundreds of binary orders of magnitude."""
+groups, odd ranks, GQA, permuted pages, value ranks above 2048, several causal
+queries a sequence (one to eight row slices), and softmax weights spread over
+hundreds of binary orders of magnitude."""
 
 import numpy as np
 import pytest
 import torch
 
-from gpu_common import TOL_REL_ROW, dev, gpu_pool_with_append, oracle_rows, row_rel_err, run_decode
+from gpu_common import (TOL_REL_ROW, dev, gpu_pool_with_append, oracle_pool, oracle_rows, row_rel_err,
+                        run_decode)
+from oracle import attention as oattn
+from oracle.bookkeeping import book_for
 from test_gpu_parity import SMALL, _all_rows, _report, _small_inputs
 from workloads.configs import custom_workload
 from workloads.inputs import make_inputs
@@ -144,3 +148,92 @@ def test_two_pass_large_value_rank(rv):
         pool = gpu_pool_with_append(inp, plan)
         out = run_decode(inp, plan, pool)
         _check_all(wl, inp, out, f"rv{rv}/{'two-pass' if passes == 2 else 'single-pass'}")
+
+
+# (case, Q): several causal queries a sequence on the two-pass kernels.  Up
+# to 32 rows take one slice (the per-wave value pass); beyond, 2 to 8 slices
+# of up to 32 rows each share one walk over the value latents (4, 6, 8 and 16
+# row tiles); mha_odd holds a one-token and an empty sequence.
+MULTI_PASS = [("singletons", 3), ("gqa_uneven", 4), ("mha_odd", 8), ("mha32_two_tiles", 2),
+              ("mha32_two_tiles", 3), ("gqa_reordered", 4), ("mha32_two_tiles", 8)]
+
+
+def _multi_plan(wl, Q, split=0, passes=2):
+    from paper_2607_24331_amd import Plan
+    p = Plan(wl.hidden, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_of_kv,
+             wl.group_rank, wl.value_rank, wl.dtype, split, queries_per_seq=Q, decode_passes=passes)
+    assert p.geometry["two_pass"] == (1 if passes == 2 else 0)
+    return p
+
+
+def _multi_check(wl, inp, plan, Q, name, scale=1.0, seed=11):
+    from paper_2607_24331_amd import decode
+    pool = gpu_pool_with_append(inp, plan)
+    qm = (np.random.default_rng(seed).standard_normal(
+        (wl.batch, Q, wl.num_q_heads, wl.head_dim)) * scale).astype(np.float32)
+    out = decode(plan, torch.from_numpy(qm).cuda(), pool, torch.from_numpy(inp.page_table).cuda(),
+                 torch.from_numpy(inp.seq_lens).cuda(), int(max(wl.seq_lens)),
+                 dev(inp.R_keys_flat, wl.dtype), dev(inp.R_value, wl.dtype))
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().astype(np.float64)
+    assert np.isfinite(got).all()
+    ref = oattn.decode_multi(qm, oracle_pool(inp), inp.page_table, wl.seq_lens, inp.R_blocks,
+                             inp.R_value, book_for(wl), chunk=None)
+    errs = []
+    for b in range(wl.batch):
+        for i in range(Q):
+            seen = oattn.visible_tokens(wl.seq_lens[b], Q, i)
+            for h in range(wl.num_q_heads):
+                if seen == 0:
+                    assert np.all(got[b, i, h] == 0)
+                else:
+                    errs.append(row_rel_err(got[b, i, h], ref[b, i, h]))
+    _report(name, errs)
+    assert max(errs) <= TOL_REL_ROW
+    return got
+
+
+@pytest.mark.parametrize("name, Q", MULTI_PASS)
+@pytest.mark.parametrize("chunked", [False, True])
+def test_two_pass_multi_query_all_rows(name, Q, chunked):
+    wl, inp, split = _small_inputs(name)
+    plan = _multi_plan(wl, Q, split if chunked else 0)
+    info = plan.launch_info(wl.batch, int(max(wl.seq_lens)))
+    assert info["kernels"] == 2
+    print(f"[two-pass] {name} Q {Q} split {split if chunked else 'auto'} {info}", flush=True)
+    _multi_check(wl, inp, plan, Q, f"two-pass/{name}/Q{Q}/{'chunked' if chunked else 'auto'}")
+
+
+@pytest.mark.parametrize("scale", [16.0, 300.0])
+def test_two_pass_multi_query_peaked_softmax(scale):
+    # per-page exponents far apart: the staged weights rescaled to running
+    # exponents that change from page to page, the accumulators with them
+    wl, inp, split = _small_inputs("gqa_reordered")
+    plan = _multi_plan(wl, 4, 64)
+    _multi_check(wl, inp, plan, 4, f"two-pass/Q4 peaked x{scale:g}", scale=scale)
+
+
+def test_two_pass_multi_query_matches_single_pass_bitwise_stable():
+    # both kernel sets on the same rows, each bitwise repeatable
+    wl, inp, split = _small_inputs("mha32_two_tiles")
+    a = _multi_check(wl, inp, _multi_plan(wl, 4, 0), 4, "two-pass/Q4")
+    b = _multi_check(wl, inp, _multi_plan(wl, 4, 0), 4, "two-pass/Q4 again")
+    assert np.array_equal(a, b)
+    c = _multi_check(wl, inp, _multi_plan(wl, 4, 256, passes=1), 4, "single-pass/Q4")
+    assert np.max(np.abs(a - c)) <= 2e-2 * np.max(np.abs(c))
+
+
+def test_two_pass_multi_query_wide_value_groups():
+    # 64 rows (four row tiles) over enough pages that a value work-group
+    # takes 32 tiles (four a wave)
+    wl = custom_workload(name="q2_rv2048", seed=2048, hidden=4096, num_q_heads=32, num_kv_heads=32,
+                         head_dim=128, group_of_kv=tuple(i // 8 for i in range(32)),
+                         group_rank=(300, 200, 100, 50), value_rank=2048, dtype="bf16", batch=2,
+                         seq_lens=(16384, 9001), prefill_lens=(16384, 9001),
+                         factor_scheme="orthonormal")
+    inp = make_inputs(wl)
+    plan = _multi_plan(wl, 2)
+    info = plan.launch_info(wl.batch, 16384)
+    assert info["kernels"] == 2 and info["head_slices"] == 2 and info["value_tiles"] == 32, info
+    print(f"[two-pass] q2_rv2048 {info}", flush=True)
+    _multi_check(wl, inp, plan, 2, "two-pass/q2_rv2048")

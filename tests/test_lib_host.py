@@ -208,20 +208,52 @@ def test_decode_path_selection():
     assert p.geometry["mfma_path"] == 1 and p.geometry["two_pass"] == 1
     assert p.geometry["head_slices"] == 2
     # value rank 4096, 32 heads, 4 queries a sequence: eight slices of 16 rows
+    # on the single-pass kernel; the two-pass kernels take the 128 rows too
     p4 = Plan(4096, 32, 32, 128, [i // 8 for i in range(32)], [300, 200, 100, 50], 4096, "bf16",
               queries_per_seq=4)
-    assert p4.geometry["mfma_path"] == 1 and p4.geometry["two_pass"] == 0
+    assert p4.geometry["mfma_path"] == 1 and p4.geometry["two_pass"] == 1
     assert p4.geometry["head_slices"] == 8
-    # an explicit single-pass plan, and a two-pass request the layer cannot take
+    # an explicit single-pass plan, and two-pass requests the layer cannot
+    # take: 512 (query, head) rows, fp32 latents
     assert Plan(*args, decode_passes=1).geometry["two_pass"] == 0
+    assert Plan(*args, queries_per_seq=8, decode_passes=2).geometry["two_pass"] == 1
     from paper_2607_24331_amd import DckvError
     with pytest.raises(DckvError, match="decode_passes"):
-        Plan(*args, queries_per_seq=2, decode_passes=2)
+        Plan(*args, queries_per_seq=16, decode_passes=2)
+    with pytest.raises(DckvError, match="decode_passes"):
+        Plan(*args[:-1], "f32", decode_passes=2)
     # explicit head slices
     wl = make_workload("mha_long_t128k")
     from paper_2607_24331_amd import Plan as P2
     p2 = P2(wl.hidden, 32, 32, 128, wl.group_of_kv, wl.group_rank, wl.value_rank, "bf16", 0, 2)
     assert p2.geometry["mfma_path"] == 1 and p2.geometry["head_slices"] == 2
+
+
+def test_launch_info_reports_the_path():
+    from paper_2607_24331_amd import Plan
+    wl = make_workload("mha_long_t128k")
+    args = (wl.hidden, 32, 32, 128, wl.group_of_kv, wl.group_rank, wl.value_rank, "bf16", 0)
+    # one query: the single-pass split kernel, one slice
+    i1 = Plan(*args).launch_info(1, 131072)
+    assert i1["kernels"] == 1 and i1["head_slices"] == 1
+    # four queries over 2048 pages: the two-pass kernels read the value part
+    # once for the four slices; chunks of at most 64 pages
+    p4 = Plan(*args, queries_per_seq=4)
+    i4 = p4.launch_info(1, 131072)
+    assert i4["kernels"] == 2 and i4["head_slices"] == 4
+    assert 0 < i4["split_tokens"] <= 64 * 64 and i4["n_split"] * i4["split_tokens"] >= 131072
+    # a short context stays on the single-pass kernel
+    assert p4.launch_info(1, 4096)["kernels"] == 1
+    assert Plan(*args, queries_per_seq=4, decode_passes=1).launch_info(1, 131072)["kernels"] == 1
+    # many sequences of long context: the chunk search starts at the fewest
+    # chunks the chunk-length cap allows, even past two work-groups a unit
+    for q in (1, 4):
+        p = Plan(*args, queries_per_seq=q, decode_passes=2)
+        for batch in (64, 256):
+            info = p.launch_info(batch, 131072)
+            assert info["kernels"] == 2 and info["split_tokens"] > 0, (q, batch, info)
+            assert info["n_split"] * info["split_tokens"] >= 131072
+            assert p.workspace_bytes(batch, 131072) > 0
 
 
 def test_queries_per_seq_plan():
