@@ -223,11 +223,11 @@ hipError_t launch_decode_t(const dckv_plan& p, const DecodeShape& sh, const floa
 // length.  One row slice: waves take pages of the chunk, a group of 4, 6 or
 // 8 tiles; the estimate is rounds x (pages a wave x (tiles + head tiles, the
 // weight loads counted at half a tile each) + a fixed cost of 4).  Several
-// slices: the eight waves walk the chunk's pages together, 1, 2 or 4 tiles a
-// wave (4 only for at most 4 row tiles, 1 and 2 for at most 8, 1 beyond);
-// the estimate, in sixteenths of a page of one tile a wave, is rounds x
-// (pages x (16 tiles + 8 + row tiles) + 64): a page's weights staged and a
-// barrier cost about half a tile, each row tile a sixteenth more.
+// slices: the eight waves walk the chunk's pages together, 2 or 1 tiles a
+// wave (1 only beyond 8 row tiles); the estimate, in sixteenths of a page
+// of one tile a wave, is rounds x (pages x (16 tiles + 8 + row tiles) + 64):
+// a page's weights staged and a barrier cost about half a tile, each row
+// tile a sixteenth more.
 static DecodeShape pass_shape(const dckv_plan& p, int32_t batch, int32_t max_context) {
   DecodeShape s{};
   s.batch = batch;
@@ -235,7 +235,7 @@ static DecodeShape pass_shape(const dckv_plan& p, int32_t batch, int32_t max_con
   s.pass = true;
   const int64_t npm = std::max<int64_t>(1, (int64_t(max_context) + DCKV_PAGE_TOKENS - 1) / DCKV_PAGE_TOKENS);
   s.npm = int32_t(npm);
-  s.unit_pages = 8;
+  s.unit_pages = kUnitPages;
   s.units_per_seq = int32_t((npm + s.unit_pages - 1) / s.unit_pages);
   const int64_t cap = pass_max_chunk_pages(p);
   const int64_t B = std::max<int32_t>(batch, 1);
@@ -243,12 +243,11 @@ static DecodeShape pass_shape(const dckv_plan& p, int32_t batch, int32_t max_con
   const bool shared = p.pass.n_slices > 1;
   std::vector<int32_t> options;
   if (!shared) options = {8, 6, 4};
-  else if (RT <= 4) options = {4, 2};
   else if (RT <= 8) options = {2, 1};
   else options = {1};
   int64_t best_cost = -1;
   for (int32_t rgt : options) {
-    const int64_t tiles = shared ? 8 * int64_t(rgt) : rgt;   // value tiles a work-group
+    const int64_t tiles = shared ? int64_t(kSharedWaves) * rgt : rgt;   // value tiles a work-group
     const int64_t nrg = (p.pass.mt_v + tiles - 1) / tiles;
     auto consider = [&](int64_t cp) {
       const int64_t nc = (npm + cp - 1) / cp;
@@ -278,8 +277,7 @@ static DecodeShape pass_shape(const dckv_plan& p, int32_t batch, int32_t max_con
   const size_t ns = 16 * size_t(RT);          // row slots
   s.off_qt = 0;
   s.off_p = align_up(size_t(batch) * p.pass.n_slices * p.pass.max_pairs * 2048, 256);
-  s.off_el = s.off_p + align_up(size_t(batch) * npm * ns * 64 * 2, 256);
-  s.off_ml = s.off_el + align_up(size_t(batch) * npm * RT * 512, 256);
+  s.off_ml = s.off_p + align_up(size_t(batch) * npm * RT * 2560, 256);   // weights and records
   const size_t rows = size_t(batch) * s.n_chunks;
   s.off_acc = s.off_ml + align_up(rows * 2 * ns * sizeof(float), 256);
   s.off_opart = s.off_acc + align_up(rows * ns * size_t(p.rv) * sizeof(float), 256);

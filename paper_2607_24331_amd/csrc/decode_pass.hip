@@ -94,34 +94,44 @@ __device__ __forceinline__ u32x4 scale8(u32x4 v, float f) {
 
 // ---------------------------------------------------------------------------
 // Score pass.  Work-group u: sequence u / units_per_seq, pages
-// [ur * unit_pages, (ur + 1) * unit_pages) of it.  The eight waves serve
+// [ur * kUnitPages, (ur + 1) * kUnitPages) of it.  The eight waves serve
 // PP = 2 / NT pages at a time: wave w takes head tile n = (w / 4) % NT and
 // 16-token row block m = w % 4 of pages pl, pl + PP, ... (pl = w / (4 NT)),
 // so the waves of a work-group stream the same pages side by side.  A
 // wave's items are, page after page, the 1 KB operands of its 16 tokens in
 // the key chunks of its tile's groups; a ring of RING loads runs ahead
-// across page boundaries.  The weights of a row block are taken relative to
-// its own integer exponent e = ceil(max over its 16 tokens), so no wave waits
-// for another.
+// across page boundaries.  Each wave keeps its pages' weights in LDS,
+// relative to the integer exponent of its 16 tokens; once every page is
+// scored, the work-group's exponent of a row is e = ceil(max over the unit's
+// scores) (the largest of those), and each wave writes its weights rescaled
+// to it by exact powers of two.  One exponent for the unit's pages lets the
+// value pass use the weights as stored, rescaling its accumulators only
+// where the exponent changes.
 //
 // With several queries a sequence the rows are cut into J slices (as for
 // the single-pass kernel): work-group (unit, slice) loads the key chunks of
 // its slice's groups, and a row of query i sees positions before
 // T_b - Q + i + 1.
 //
-// Outputs per (sequence b, page pg of it, row tile t = slice * NT + n):
-//   pbuf   2 KB: the weights as the value MFMA's B operand, 16 heads x 64
+// Outputs per (sequence b, page pg of it): a block of RT x 2560 bytes (RT =
+// J NT row tiles) at (b * npm + pg) * RT * 2560 holding, for row tile t =
+// slice * NT + n,
+//   at t * 2 KB: the weights as the value MFMA's B operand, 16 rows x 64
 //          tokens: k-step ks (tokens 32ks..32ks+31) at ks * 1024 bytes, lane
-//          L = 16 * (t%32 / 8) + head at L * 16, 8 tokens a lane
-//   elbuf  512 B: e and l of row slot j and row block m at floats 8j + m and
-//          8j + 4 + m, l the sum of the block's rounded weights
+//          L = 16 * (token%32 / 8) + row at L * 16, 8 tokens a lane
+//   at RT * 2 KB + t * 512: e and l of row slot j and row block m at floats
+//          8j + m and 8j + 4 + m: e the unit's exponent of the row (the same
+//          for every block and page of the unit; -inf for a row with no
+//          visible token in the unit), l the sum of the block's weights as
+//          stored
 template <int NT, int RING>
 __global__ __launch_bounds__(512, 1) void score_pages(
     const u32x4* __restrict__ qblk_ws, const bf16* __restrict__ pool, int64_t num_pages,
     const int32_t* __restrict__ page_table, int max_pages, const int32_t* __restrict__ seq_lens,
-    int max_context, int unit_pages, int units_per_seq, int n_units, int npm, int RK,
-    int64_t page_elems, uint32_t* __restrict__ pbuf, float* __restrict__ elbuf, MfmaTables mt) {
+    int max_context, int units_per_seq, int n_units, int npm, int RK, int64_t page_elems,
+    uint32_t* __restrict__ pw, MfmaTables mt) {
   constexpr int PP = 2 / NT;                   // pages side by side
+  constexpr int unit_pages = kUnitPages;
   extern __shared__ __align__(16) unsigned char smem[];
   // the J slices of a page range run side by side on one XCD (block ids
   // equal mod 8), so a key chunk two slices load comes the second time from
@@ -166,7 +176,7 @@ __global__ __launch_bounds__(512, 1) void score_pages(
   T_b = T_b < 0 ? 0 : (T_b > max_context ? max_context : T_b);
   const int np = (T_b + 63) >> 6;
   const int p1 = min(np, p0 + unit_pages);
-  const int nmine = max(0, (p1 - p0 - pl + PP - 1) / PP);       // this wave's pages (<= 64)
+  const int nmine = max(0, (p1 - p0 - pl + PP - 1) / PP);       // this wave's pages (<= 8)
   const int total = nmine * nch;
   const int lim = hrow < 0 ? 0 : T_b - mt.queries + hrow / mt.q_heads + 1;
 
@@ -215,7 +225,19 @@ __global__ __launch_bounds__(512, 1) void score_pages(
   floatx4 S = floatx4{0.f, 0.f, 0.f, 0.f};
   u32x4 bhi = qblk[(pair0 * 2 + 0) * 64 + lane], blo = qblk[(pair0 * 2 + 1) * 64 + lane];
 
-  // the weights of this wave's 16 tokens of page k, from S
+  // LDS after the query blocks: per wave and page (at most kUnitPages) the
+  // weights, 8 bytes a lane, then per wave, page and row the exponent and sum
+  const size_t stage0 = size_t(mt.max_pairs) * 2048;
+  uint2* pst = reinterpret_cast<uint2*>(smem + stage0) + w * kUnitPages * 64;
+  float* est = reinterpret_cast<float*>(smem + stage0 + 8 * kUnitPages * 512);
+  float* lst = est + 8 * kUnitPages * 16;
+  if (lq == 0) {
+#pragma unroll
+    for (int k = 0; k < kUnitPages; ++k) est[(w * kUnitPages + k) * 16 + lr] = -INFINITY;
+  }
+
+  // the weights of this wave's 16 tokens of page k, from S, relative to
+  // their own exponent, into LDS
   auto epilogue = [&](int k) {
     const int pg = p0 + pl + PP * k;
     const bool pvalid = __builtin_amdgcn_readlane(pid_tbl, min(k, 63)) >= 0;
@@ -243,15 +265,11 @@ __global__ __launch_bounds__(512, 1) void score_pages(
       }
       pk[v2] = word;
     }
-    // tokens 16m + 4lq .. +3: k-step m/2, operand lane 16 * (2(m%2) + lq/2) + lr
-    const int64_t tile = (int64_t(b) * npm + pg) * RT + slice * NT + n;
-    uint32_t* blk = pbuf + tile * 512;
-    const int L = 16 * (2 * (m & 1) + (lq >> 1)) + lr;
-    *reinterpret_cast<uint2*>(blk + (m >> 1) * 256 + L * 4 + 2 * (lq & 1)) = uint2{pk[0], pk[1]};
+    pst[k * 64 + lane] = uint2{pk[0], pk[1]};
     psum = wave_sum16(psum);
     if (lq == 0) {
-      elbuf[tile * 128 + 8 * lr + m] = e;
-      elbuf[tile * 128 + 8 * lr + 4 + m] = psum;
+      est[(w * kUnitPages + k) * 16 + lr] = e;
+      lst[(w * kUnitPages + k) * 16 + lr] = psum;
     }
     S = floatx4{0.f, 0.f, 0.f, 0.f};
   };
@@ -284,6 +302,43 @@ __global__ __launch_bounds__(512, 1) void score_pages(
 #pragma unroll
   for (int s = 0; s < RING; ++s)
     if (base + s < total) consume(ring[s]);
+
+  // the unit's exponent of this lane's row: the largest over the waves of
+  // its tile and their pages
+  __syncthreads();
+  float eu = -INFINITY;
+#pragma unroll
+  for (int ww = 0; ww < 8; ++ww) {
+    if (((ww >> 2) % NT) == n) {
+#pragma unroll
+      for (int k = 0; k < kUnitPages; ++k) eu = fmaxf(eu, est[(ww * kUnitPages + k) * 16 + lr]);
+    }
+  }
+  // this wave's pages, rescaled to it: tokens 16m + 4lq .. +3 go to k-step
+  // m/2, operand lane 16 * (2(m%2) + lq/2) + lr
+  const int L = 16 * (2 * (m & 1) + (lq >> 1)) + lr;
+  for (int k = 0; k < nmine; ++k) {
+    const int pg = p0 + pl + PP * k;
+    const float ep = est[(w * kUnitPages + k) * 16 + lr];
+    const float f = pow2_rel(ep, eu);                  // 0 for a page with no visible token
+    const uint2 v = pst[k * 64 + lane];
+    uint32_t pk[2] = {v.x, v.y};
+#pragma unroll
+    for (int d = 0; d < 2; ++d) {
+      const float lo = __uint_as_float(pk[d] << 16) * f;
+      const float hi = __uint_as_float(pk[d] & 0xFFFF0000u) * f;
+      pk[d] = (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xFFFF0000u);
+    }
+    uint32_t* pblk = pw + (int64_t(b) * npm + pg) * RT * 640;   // 2560 bytes a row tile
+    const int ti = slice * NT + n;
+    *reinterpret_cast<uint2*>(pblk + ti * 512 + (m >> 1) * 256 + L * 4 + 2 * (lq & 1)) =
+        uint2{pk[0], pk[1]};
+    if (lq == 0) {
+      float* rec = reinterpret_cast<float*>(pblk + RT * 512 + ti * 128);
+      rec[8 * lr + m] = eu;
+      rec[8 * lr + 4 + m] = lst[(w * kUnitPages + k) * 16 + lr] * f;
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -303,8 +358,8 @@ __global__ __launch_bounds__(W * 64, 1) void value_pages(
     const bf16* __restrict__ pool, int64_t num_pages, const int32_t* __restrict__ page_table,
     int max_pages, const int32_t* __restrict__ seq_lens, int max_context, int chunk_pages,
     int n_chunks, int n_rg, int batch, int npm, int rv, int mt_v, int64_t page_elems,
-    int64_t value_base, const u32x4* __restrict__ pbuf, const u32x4* __restrict__ elbuf,
-    float* __restrict__ vpart, float* __restrict__ vel) {
+    int64_t value_base, const u32x4* __restrict__ pw, float* __restrict__ vpart,
+    float* __restrict__ vel) {
   constexpr int NH = 16 * NT;
   constexpr int P0 = 2 * NT;                        // first weight item
   constexpr int V0 = 4 * NT;                        // first value item
@@ -352,10 +407,11 @@ __global__ __launch_bounds__(W * 64, 1) void value_pages(
         kRsrcWord3);
   };
   auto issue = [&](int s) -> u32x4 {
-    if (s < P0) return elbuf[((seq_page0 + ppg) * NT + (s >> 1)) * 32 + 2 * lr + (s & 1)];
+    const u32x4* pblk = pw + (seq_page0 + ppg) * NT * 160;
+    if (s < P0) return pblk[NT * 128 + (s >> 1) * 32 + 2 * lr + (s & 1)];
     if (s < V0) {
       const int n = (s - P0) >> 1, ks = (s - P0) & 1;
-      return pbuf[((seq_page0 + ppg) * NT + n) * 128 + ks * 64 + lane];
+      return pblk[n * 128 + ks * 64 + lane];
     }
     const int i = (s - V0) >> 1, ks = (s - V0) & 1;
     const int o = 2 * (int(value_base) + 1024 * (mt0 + i) + 512 * ks) + lane_val;
@@ -483,30 +539,32 @@ __global__ __launch_bounds__(W * 64, 1) void value_pages(
 
 // ---------------------------------------------------------------------------
 // Value pass for several row slices (several queries a sequence).  Work-group
-// (sequence b, chunk c, rank group g): the eight waves walk the chunk's pages
-// together, wave w owning value tiles g * 8 * RGTW + w * RGTW .. + RGTW - 1
-// against all RT row tiles, so each value latent byte is read once.  The
-// weights of a page are staged in LDS already rescaled to the running
-// exponents: thread i of the staging holds weight operand element i (row
-// tile t, k-step, operand lane) of every page and keeps the running exponent
-// E of that element's row slot (the same in every thread holding that slot:
-// the same records in the same order), and the holder of k-step 0, lanes
-// 0..15 also keeps the slot's running sum L and stages the factor 2^(E_old -
-// E_new) by which the waves rescale their accumulators.  Two buffers, one
-// barrier a page: the next page's weights load while the current one is
-// used; a wave's value loads run DP pages ahead.
+// (sequence b, chunk c, rank group g): the W waves walk the chunk's pages
+// together, wave w owning value tiles g * W * RGTW + w * RGTW .. + RGTW - 1
+// against all RT row tiles, so each value latent byte is read once.  A
+// page's weights and records are staged in LDS as stored (two buffers, one
+// barrier a page); a wave's value loads and the next page's staging loads
+// run DP pages ahead.  The weights of a row are relative to 2^e, e its exponent on
+// that page (one for all pages of a score unit).  A wave keeps per row slot
+// a base exponent B, its accumulators and the sum L being relative to 2^B:
+// a page with another exponent moves B to it, the accumulators and L
+// multiplied by 2^(B_old - B), an exact power of two above or below 1.  B
+// stays within 64 of the largest exponent met, so the accumulators stay far
+// from overflow: a page whose exponent is further below (all its weights
+// under 2^-64 of the row's largest) is left out for that row, its weights
+// zeroed in LDS before use.  All waves take the same B from the same
+// records.
 // Partials as value_pages, over NS = 16 RT row slots; no sums across waves.
-template <int RTMAX, int RGTW, int DP>
-__global__ __launch_bounds__(512, 1) void value_shared(
+template <int W, int RTMAX, int RGTW, int DP>
+__global__ __launch_bounds__(W * 64, 1) void value_shared(
     const bf16* __restrict__ pool, int64_t num_pages, const int32_t* __restrict__ page_table,
     int max_pages, const int32_t* __restrict__ seq_lens, int max_context, int chunk_pages,
     int n_chunks, int n_rg, int batch, int npm, int rv, int mt_v, int64_t page_elems,
-    int64_t value_base, int RT, const u32x4* __restrict__ pbuf, const u32x4* __restrict__ elbuf,
-    float* __restrict__ vpart, float* __restrict__ vel) {
-  constexpr int W = 8;
+    int64_t value_base, int RT, const u32x4* __restrict__ pw, float* __restrict__ vpart,
+    float* __restrict__ vel) {
+  constexpr int NTH = W * 64;
   constexpr int IP = 2 * RGTW;                      // value loads a page a wave
-  constexpr int RING = DP * IP;
-  constexpr int SV = (RTMAX * 128 + 511) / 512;     // weight elements a staging thread
+  constexpr int SV = (RTMAX * 160 + NTH - 1) / NTH; // staged 16-byte loads a thread a page
   extern __shared__ __align__(16) unsigned char smem[];
   const int Lb = blockIdx.x;
   const int xcd = Lb & 7, qd = Lb >> 3;
@@ -526,52 +584,53 @@ __global__ __launch_bounds__(512, 1) void value_shared(
   T_b = T_b < 0 ? 0 : (T_b > max_context ? max_context : T_b);
   const int np = (T_b + 63) >> 6;
   const int npg = max(0, min(np, g0 + chunk_pages) - g0);   // the chunk's pages
+  const int last = max(npg - 1, 0);
   const int pid_tbl = (pt >= 0 && pt < num_pages) ? pt : -1;
   const int mt0 = rg * W * RGTW + w * RGTW;          // this wave's first value tile
 
-  // LDS, two buffers: weights [RT][2][64] u32x4, then factors [NS] floats
-  const int nw = RT * 128;
-  u32x4* wbuf = reinterpret_cast<u32x4*>(smem);
-  float* fbuf = reinterpret_cast<float*>(wbuf + 2 * nw);
-  const u32x4* pb0 = pbuf + int64_t(b) * npm * RT * 128;
-  const u32x4* eb0 = elbuf + int64_t(b) * npm * RT * 32;
-  u32x4 sw[SV], se[SV], sl[SV];                     // raw weights, e and l records of the slot
-  float Er[SV], Lr[SV];
+  // a staged page: weights [RT][2][64] then records [NS][8] (e0..e3, l0..l3)
+  const int nst = RT * 160;
+  u32x4* lbuf = reinterpret_cast<u32x4*>(smem);     // two pages
+  // the sequence's weight blocks (RT * 2560 bytes a page) through a buffer
+  // descriptor: one offset register a staged item, the page in soffset
+  const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<u32x4*>(pw + int64_t(b) * npm * RT * 160), 0, npm * RT * 2560, kRsrcWord3);
+  // the holder of a slot's l record keeps the slot's base exponent, largest
+  // exponent and sum (the same rule as the waves', on the same records)
+  float sB[SV], sE[SV], sL[SV];
 #pragma unroll
   for (int k = 0; k < SV; ++k) {
-    Er[k] = -INFINITY;
-    Lr[k] = 0.f;
+    sB[k] = -INFINITY;
+    sE[k] = -INFINITY;
+    sL[k] = 0.f;
   }
-  auto stage_load = [&](int pg) {                   // pg < npm: loads at clamped indices
-#pragma unroll
-    for (int k = 0; k < SV; ++k) {
-      const int i = min(tid + 512 * k, nw - 1);
-      const int slot = 16 * (i >> 7) + (i & 15);
-      sw[k] = pb0[int64_t(pg) * RT * 128 + i];
-      se[k] = eb0[int64_t(pg) * RT * 32 + 2 * slot];
-      sl[k] = eb0[int64_t(pg) * RT * 32 + 2 * slot + 1];
-    }
+  auto stage_item = [&](int k, int pg) -> u32x4 {   // pg < npm
+    const int i = min(tid + NTH * k, nst - 1);
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(prs, 16 * i, pg * RT * 2560, 0));
   };
-  auto stage_store = [&](int buf) {
+  auto stage_store = [&](const u32x4* sv, int buf) {
 #pragma unroll
     for (int k = 0; k < SV; ++k) {
-      const int i = tid + 512 * k;
-      if (i < nw) {
-        const float4 ev = __builtin_bit_cast(float4, se[k]);
-        const float En = fmaxf(Er[k], fmaxf(fmaxf(ev.x, ev.y), fmaxf(ev.z, ev.w)));
-        const float f0 = pow2_rel(ev.x, En), f1 = pow2_rel(ev.y, En);
-        const float f2 = pow2_rel(ev.z, En), f3 = pow2_rel(ev.w, En);
-        // operand lane L holds tokens 32 ks + 8 (L / 16) ..: row block 2 ks + L / 32
-        const int ks = (i >> 6) & 1, hi = (i >> 5) & 1;
-        const float f = ks ? (hi ? f3 : f2) : (hi ? f1 : f0);
-        wbuf[buf * nw + i] = scale8(sw[k], f);
-        if ((i & 127) < 16) {                       // k-step 0, lanes 0..15: slot 16 t + i % 16
-          const float4 lv = __builtin_bit_cast(float4, sl[k]);
-          const float fa = Er[k] == -INFINITY ? 1.f : pow2_rel(Er[k], En);
-          Lr[k] = Lr[k] * fa + (((lv.x * f0 + lv.y * f1) + lv.z * f2) + lv.w * f3);
-          fbuf[buf * NS + 16 * (i >> 7) + (i & 15)] = fa;
+      const int i = tid + NTH * k;
+      // element i ^ 1 is held by lane ^ 1: for an l record, the e record
+      const float ep = __shfl_xor(__uint_as_float(sv[k].x), 1);
+      if (i < nst) {
+        lbuf[buf * nst + i] = sv[k];
+        if (i >= RT * 128 && (i & 1) && ep != -INFINITY) {
+          const float4 lv = __builtin_bit_cast(float4, sv[k]);
+          const float sum = (lv.x + lv.y) + (lv.z + lv.w);
+          if (ep == sB[k]) {
+            sL[k] += sum;
+          } else {
+            const float em = fmaxf(sE[k], ep);
+            if (ep >= em - 64.f) {
+              const float fa = sB[k] == -INFINITY ? 1.f : pow2_rel(sB[k], ep);
+              sL[k] = sL[k] * fa + sum;
+              sB[k] = ep;
+              sE[k] = em;
+            }
+          }
         }
-        Er[k] = En;
       }
     }
   };
@@ -596,15 +655,25 @@ __global__ __launch_bounds__(512, 1) void value_shared(
                                          rsrc, ok ? o : kOutOfRange, 0, kNonTemporal));
   };
 
-  u32x4 ring[RING];
-  stage_load(g0);
+  // ring slot d (page k = d mod DP): the value loads of page k and the
+  // staging loads of page k + 1, both issued DP pages ahead
+  u32x4 ring[DP][IP + SV];
+  auto fill = [&](int d, int k) {
+    set_page(k);
 #pragma unroll
-  for (int d = 0; d < DP; ++d) {
-    set_page(d);
+    for (int s = 0; s < IP; ++s) ring[d][s] = issue(s);
+    const int pg = g0 + min(k + 1, last);
 #pragma unroll
-    for (int s = 0; s < IP; ++s) ring[d * IP + s] = issue(s);
+    for (int s = 0; s < SV; ++s) ring[d][IP + s] = stage_item(s, pg);
+  };
+  {
+    u32x4 s0[SV];
+#pragma unroll
+    for (int s = 0; s < SV; ++s) s0[s] = stage_item(s, g0);
+#pragma unroll
+    for (int d = 0; d < DP; ++d) fill(d, d);
+    if (npg > 0) stage_store(s0, 0);
   }
-  if (npg > 0) stage_store(0);
   __syncthreads();
 
   floatx4 acc[RGTW][RTMAX];
@@ -612,50 +681,97 @@ __global__ __launch_bounds__(512, 1) void value_shared(
   for (int i = 0; i < RGTW; ++i)
 #pragma unroll
     for (int t = 0; t < RTMAX; ++t) acc[i][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float Bx[RTMAX], Em[RTMAX];                      // base and largest exponent per row slot
+#pragma unroll
+  for (int t = 0; t < RTMAX; ++t) {
+    Bx[t] = -INFINITY;
+    Em[t] = -INFINITY;
+  }
 
-  // page k of the chunk, its value loads in ring slots d * IP ..
+  // page k of the chunk, ring slot d = k mod DP, staged in buffer k % 2
   auto page = [&](int k, int d) {
     const int cur = k & 1;
-    const bool more = k + 1 < npg;
-    stage_load(g0 + (more ? k + 1 : k));            // the next page's weights, in flight
-    const u32x4* lb = wbuf + cur * nw;
-    float fa[RTMAX];
-    bool resc = false;
+    const u32x4* lb = lbuf + cur * nst;
+    const float* rec = reinterpret_cast<const float*>(lb + RT * 128);
+    // the page's exponents of this lane's row slots, read together; the
+    // usual page (the same exponents as the last: a score unit spans eight
+    // pages) changes nothing
+    float ev[RTMAX];
 #pragma unroll
-    for (int t = 0; t < RTMAX; ++t) {
-      fa[t] = t < RT ? fbuf[cur * NS + 16 * t + lr] : 1.f;
-      resc = resc || fa[t] != 1.f;
+    for (int t = 0; t < RTMAX; ++t) ev[t] = rec[(16 * min(t, RT - 1) + lr) * 8];
+    bool same = true;
+#pragma unroll
+    for (int t = 0; t < RTMAX; ++t) same = same && (t >= RT || ev[t] == Bx[t]);
+    uint32_t dropped = 0;                           // row tiles left out
+    if (!__all(same)) {
+      bool resc = false;
+      float fa[RTMAX];
+#pragma unroll
+      for (int t = 0; t < RTMAX; ++t) {
+        fa[t] = 1.f;
+        const float ep = ev[t];
+        if (t < RT && ep != -INFINITY) {            // else the row's weights are zero
+          const float em = fmaxf(Em[t], ep);
+          if (ep >= em - 64.f) {
+            fa[t] = Bx[t] == -INFINITY ? 1.f : pow2_rel(Bx[t], ep);
+            Bx[t] = ep;
+            Em[t] = em;
+          } else {
+            dropped |= 1u << t;                     // below 2^-64 of the row's largest weights
+          }
+        }
+        resc = resc || fa[t] != 1.f;
+      }
+      if (__any(resc)) {
+#pragma unroll
+        for (int i = 0; i < RGTW; ++i)
+#pragma unroll
+          for (int t = 0; t < RTMAX; ++t) acc[i][t] *= fa[t];
+      }
     }
-    if (__any(resc)) {
+    if (__any(dropped != 0)) {
+      // each wave zeroes its own lanes' operand elements of the dropped rows
+      // before reading them (all waves write the same zeros, and a lane's
+      // read follows its own write)
+      u32x4* lw = lbuf + cur * nst;
 #pragma unroll
-      for (int i = 0; i < RGTW; ++i)
-#pragma unroll
-        for (int t = 0; t < RTMAX; ++t) acc[i][t] *= fa[t];
+      for (int t = 0; t < RTMAX; ++t) {
+        if (t < RT && ((dropped >> t) & 1u)) {
+          lw[t * 128 + lane] = u32x4{0u, 0u, 0u, 0u};
+          lw[t * 128 + 64 + lane] = u32x4{0u, 0u, 0u, 0u};
+        }
+      }
     }
     const int nval = min(64, T_b - 64 * (g0 + k));
     const int keep0 = min(8, max(0, nval - 8 * lq));
     const int keep1 = min(8, max(0, nval - 32 - 8 * lq));
+    // weight operands (k-step, row tile) in order, BQ LDS reads ahead of
+    // their products
+    constexpr int NB = 2 * RTMAX, BQ = 3;
+    auto bload = [&](int j) { return lb[min(j % RTMAX, RT - 1) * 128 + (j / RTMAX) * 64 + lane]; };
+    u32x4 bq[BQ];
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      u32x4 a[RGTW];
+    for (int j = 0; j < BQ; ++j) bq[j] = bload(j);
+    u32x4 a[RGTW];
 #pragma unroll
-      for (int i = 0; i < RGTW; ++i) {
-        a[i] = ring[d * IP + 2 * i + ks];
-        if (nval < 64) a[i] = keep_first(a[i], ks ? keep1 : keep0);
-      }
+    for (int j = 0; j < NB; ++j) {
+      const int ks = j / RTMAX, t = j % RTMAX;
+      if (t == 0) {
 #pragma unroll
-      for (int t = 0; t < RTMAX; ++t) {
-        if (t < RT) {
-          const u32x4 B = lb[t * 128 + ks * 64 + lane];
-#pragma unroll
-          for (int i = 0; i < RGTW; ++i) acc[i][t] = mfma(a[i], B, acc[i][t]);
+        for (int i = 0; i < RGTW; ++i) {
+          a[i] = ring[d][2 * i + ks];
+          if (nval < 64) a[i] = keep_first(a[i], ks ? keep1 : keep0);
         }
       }
-    }
-    set_page(k + DP);                                // refill this page's slots
+      const u32x4 B = bq[j % BQ];
+      if (j + BQ < NB) bq[j % BQ] = bload(j + BQ);
+      if (t < RT) {
 #pragma unroll
-    for (int s = 0; s < IP; ++s) ring[d * IP + s] = issue(s);
-    if (more) stage_store(cur ^ 1);
+        for (int i = 0; i < RGTW; ++i) acc[i][t] = mfma(a[i], B, acc[i][t]);
+      }
+    }
+    if (k + 1 < npg) stage_store(&ring[d][IP], cur ^ 1);   // page k + 1, loaded DP pages back
+    fill(d, k + DP);
     __syncthreads();
   };
   int k0 = 0;
@@ -684,11 +800,11 @@ __global__ __launch_bounds__(512, 1) void value_shared(
   if (rg == 0) {
 #pragma unroll
     for (int k = 0; k < SV; ++k) {
-      const int i = tid + 512 * k;
-      if (i < nw && (i & 127) < 16) {
-        const int slot = 16 * (i >> 7) + (i & 15);
-        vel[int64_t(cidx) * 2 * NS + slot] = Er[k];
-        vel[int64_t(cidx) * 2 * NS + NS + slot] = Lr[k];
+      const int i = tid + NTH * k;
+      if (i < nst && i >= RT * 128 && (i & 1)) {
+        const int slot = (i - RT * 128) >> 1;
+        vel[int64_t(cidx) * 2 * NS + slot] = sB[k];
+        vel[int64_t(cidx) * 2 * NS + NS + slot] = sL[k];
       }
     }
   }
@@ -884,12 +1000,14 @@ __global__ __launch_bounds__(256) void upproj_rows(const float* __restrict__ ame
 }  // namespace
 
 size_t pass_score_lds_bytes(const dckv_plan& p) {
-  return std::max<size_t>(size_t(p.pass.max_pairs) * 2048, kScoreMinLds);
+  // query blocks, then each wave's pages: 512 B of weights and 128 B of
+  // exponents and sums a page
+  return std::max<size_t>(size_t(p.pass.max_pairs) * 2048 + 8 * kUnitPages * (512 + 128), kScoreMinLds);
 }
 
 size_t pass_value_lds_bytes(const dckv_plan& p, int rgt) {
-  if (p.pass.n_slices > 1)   // two pages' weights and factors, 2 KB + 64 B a row tile
-    return size_t(2) * p.pass.n_slices * p.pass.nt * (2048 + 64);
+  if (p.pass.n_slices > 1)   // two pages' weights and records, 2.5 KB a row tile
+    return size_t(2) * p.pass.n_slices * p.pass.nt * 2560;
   const int nh = 16 * p.pass.nt, W = 8;
   return size_t(2) * W * nh * 4 + size_t(W) * rgt * p.pass.nt * 64 * 16;
 }
@@ -906,8 +1024,8 @@ int pass_max_chunk_pages(const dckv_plan& p) {
 template <int NT, int RGT>
 hipError_t launch_value(const dckv_plan& p, const DecodeShape& sh, const void* pool,
                         int64_t num_pages, const int32_t* page_table, int32_t max_pages,
-                        const int32_t* seq_lens, const u32x4* pbuf, const u32x4* elbuf, float* vpart,
-                        float* vel, hipStream_t stream) {
+                        const int32_t* seq_lens, const u32x4* pw, float* vpart, float* vel,
+                        hipStream_t stream) {
   auto kern = value_pages<8, NT, RGT>;
   const size_t lds = pass_value_lds_bytes(p, RGT);
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -919,22 +1037,22 @@ hipError_t launch_value(const dckv_plan& p, const DecodeShape& sh, const void* p
     hipExtLaunchKernelGGL(kern, grid, dim3(512), uint32_t(lds), stream, p.prof_before, p.prof_after,
                           0u, static_cast<const bf16*>(pool), num_pages, page_table, max_pages,
                           seq_lens, sh.max_context, sh.chunk_pages, sh.n_chunks, sh.n_rgroups,
-                          sh.batch, sh.npm, p.rv, p.pass.mt_v, p.page_elems, p.value_base, pbuf,
-                          elbuf, vpart, vel);
+                          sh.batch, sh.npm, p.rv, p.pass.mt_v, p.page_elems, p.value_base, pw,
+                          vpart, vel);
   else
     hipLaunchKernelGGL(kern, grid, dim3(512), lds, stream, static_cast<const bf16*>(pool),
                        num_pages, page_table, max_pages, seq_lens, sh.max_context, sh.chunk_pages,
                        sh.n_chunks, sh.n_rgroups, sh.batch, sh.npm, p.rv, p.pass.mt_v,
-                       p.page_elems, p.value_base, pbuf, elbuf, vpart, vel);
+                       p.page_elems, p.value_base, pw, vpart, vel);
   return hipGetLastError();
 }
 
-template <int RTMAX, int RGTW, int DP>
+template <int W, int RTMAX, int RGTW, int DP>
 hipError_t launch_shared(const dckv_plan& p, const DecodeShape& sh, const void* pool,
                          int64_t num_pages, const int32_t* page_table, int32_t max_pages,
-                         const int32_t* seq_lens, const u32x4* pbuf, const u32x4* elbuf,
-                         float* vpart, float* vel, hipStream_t stream) {
-  auto kern = value_shared<RTMAX, RGTW, DP>;
+                         const int32_t* seq_lens, const u32x4* pw, float* vpart, float* vel,
+                         hipStream_t stream) {
+  auto kern = value_shared<W, RTMAX, RGTW, DP>;
   const size_t lds = pass_value_lds_bytes(p, RGTW);
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
@@ -943,38 +1061,37 @@ hipError_t launch_shared(const dckv_plan& p, const DecodeShape& sh, const void* 
   const dim3 grid(unsigned(8 * sh.n_rgroups * ((bc + 7) / 8)));
   const int RT = p.pass.n_slices * p.pass.nt;
   if (p.prof_before && p.prof_after)
-    hipExtLaunchKernelGGL(kern, grid, dim3(512), uint32_t(lds), stream, p.prof_before, p.prof_after,
+    hipExtLaunchKernelGGL(kern, grid, dim3(W * 64), uint32_t(lds), stream, p.prof_before, p.prof_after,
                           0u, static_cast<const bf16*>(pool), num_pages, page_table, max_pages,
                           seq_lens, sh.max_context, sh.chunk_pages, sh.n_chunks, sh.n_rgroups,
-                          sh.batch, sh.npm, p.rv, p.pass.mt_v, p.page_elems, p.value_base, RT, pbuf,
-                          elbuf, vpart, vel);
+                          sh.batch, sh.npm, p.rv, p.pass.mt_v, p.page_elems, p.value_base, RT, pw,
+                          vpart, vel);
   else
-    hipLaunchKernelGGL(kern, grid, dim3(512), lds, stream, static_cast<const bf16*>(pool), num_pages,
+    hipLaunchKernelGGL(kern, grid, dim3(W * 64), lds, stream, static_cast<const bf16*>(pool), num_pages,
                        page_table, max_pages, seq_lens, sh.max_context, sh.chunk_pages, sh.n_chunks,
                        sh.n_rgroups, sh.batch, sh.npm, p.rv, p.pass.mt_v, p.page_elems, p.value_base,
-                       RT, pbuf, elbuf, vpart, vel);
+                       RT, pw, vpart, vel);
   return hipGetLastError();
 }
 
-// The shared-weights value pass for RT row tiles and RGTW value tiles a wave.
+// The shared-weights value pass: RGTW (sh.rgt) value tiles a wave, for up
+// to 8 or 16 row tiles.
 hipError_t launch_value_shared(const dckv_plan& p, const DecodeShape& sh, const void* pool,
                                int64_t num_pages, const int32_t* page_table, int32_t max_pages,
-                               const int32_t* seq_lens, const u32x4* pbuf, const u32x4* elbuf,
-                               float* vpart, float* vel, hipStream_t stream) {
+                               const int32_t* seq_lens, const u32x4* pw, float* vpart,
+                               float* vel, hipStream_t stream) {
   const int RT = p.pass.n_slices * p.pass.nt;
 #define DCKV_SHARED(RTMAX, RGTW, DP) \
-  launch_shared<RTMAX, RGTW, DP>(p, sh, pool, num_pages, page_table, max_pages, seq_lens, pbuf, elbuf, vpart, vel, stream)
-  if (RT <= 4) return sh.rgt == 4 ? DCKV_SHARED(4, 4, 2) : DCKV_SHARED(4, 2, 4);
-  if (RT <= 8) return sh.rgt == 2 ? DCKV_SHARED(8, 2, 3) : DCKV_SHARED(8, 1, 6);
+  launch_shared<kSharedWaves, RTMAX, RGTW, DP>(p, sh, pool, num_pages, page_table, max_pages, seq_lens, pw, vpart, vel, stream)
+  if (RT <= 8) return sh.rgt == 2 ? DCKV_SHARED(8, 2, 2) : DCKV_SHARED(8, 1, 8);
+  return DCKV_SHARED(16, 1, 4);
 #undef DCKV_SHARED
-  return launch_shared<16, 1, 3>(p, sh, pool, num_pages, page_table, max_pages, seq_lens, pbuf,
-                                 elbuf, vpart, vel, stream);
 }
 
 template <int NT, int RING>
 hipError_t launch_score_r(const dckv_plan& p, const DecodeShape& sh, const u32x4* qblk,
                           const void* pool, int64_t num_pages, const int32_t* page_table,
-                          int32_t max_pages, const int32_t* seq_lens, uint32_t* pbuf, float* elbuf,
+                          int32_t max_pages, const int32_t* seq_lens, uint32_t* pw,
                           hipStream_t stream) {
   auto kern = score_pages<NT, RING>;
   const size_t lds = pass_score_lds_bytes(p);
@@ -984,19 +1101,19 @@ hipError_t launch_score_r(const dckv_plan& p, const DecodeShape& sh, const u32x4
   const int n_units = sh.batch * sh.units_per_seq;
   hipLaunchKernelGGL(kern, dim3(8 * p.pass.n_slices * ((n_units + 7) / 8)), dim3(512), lds, stream, qblk,
                      static_cast<const bf16*>(pool), num_pages, page_table, max_pages, seq_lens,
-                     sh.max_context, sh.unit_pages, sh.units_per_seq, n_units, sh.npm, p.RK,
-                     p.page_elems, pbuf, elbuf, p.pass);
+                     sh.max_context, sh.units_per_seq, n_units, sh.npm, p.RK, p.page_elems, pw,
+                     p.pass);
   return hipGetLastError();
 }
 
 template <int NT>
 hipError_t launch_score(const dckv_plan& p, const DecodeShape& sh, const u32x4* qblk,
                         const void* pool, int64_t num_pages, const int32_t* page_table,
-                        int32_t max_pages, const int32_t* seq_lens, uint32_t* pbuf, float* elbuf,
+                        int32_t max_pages, const int32_t* seq_lens, uint32_t* pw,
                         hipStream_t stream) {
   switch (p.pass_ring) {
-    case 16: return launch_score_r<NT, 16>(p, sh, qblk, pool, num_pages, page_table, max_pages, seq_lens, pbuf, elbuf, stream);
-    case 32: return launch_score_r<NT, 32>(p, sh, qblk, pool, num_pages, page_table, max_pages, seq_lens, pbuf, elbuf, stream);
+    case 16: return launch_score_r<NT, 16>(p, sh, qblk, pool, num_pages, page_table, max_pages, seq_lens, pw, stream);
+    case 32: return launch_score_r<NT, 32>(p, sh, qblk, pool, num_pages, page_table, max_pages, seq_lens, pw, stream);
   }
   return hipErrorInvalidValue;
 }
@@ -1032,25 +1149,23 @@ hipError_t launch_decode_pass(const dckv_plan& p, const DecodeShape& sh, const f
                               const void* R_value, float* out, void* workspace, hipStream_t stream) {
   char* ws = static_cast<char*>(workspace);
   u32x4* qt = reinterpret_cast<u32x4*>(ws + sh.off_qt);
-  uint32_t* pbuf = reinterpret_cast<uint32_t*>(ws + sh.off_p);
-  float* elbuf = reinterpret_cast<float*>(ws + sh.off_el);
+  uint32_t* pw = reinterpret_cast<uint32_t*>(ws + sh.off_p);
   float* vpart = reinterpret_cast<float*>(ws + sh.off_acc);
   float* vel = reinterpret_cast<float*>(ws + sh.off_ml);
   float* amerged = reinterpret_cast<float*>(ws + sh.off_opart);
   hipError_t e = launch_fold(p, p.pass, sh.batch, q, R_keys, qt, stream);
   if (e != hipSuccess) return e;
   e = p.pass.nt == 1 ? launch_score<1>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens,
-                                       pbuf, elbuf, stream)
+                                       pw, stream)
                      : launch_score<2>(p, sh, qt, pool, num_pages, page_table, max_pages, seq_lens,
-                                       pbuf, elbuf, stream);
+                                       pw, stream);
   if (e != hipSuccess) return e;
-  const u32x4* pb4 = reinterpret_cast<const u32x4*>(pbuf);
-  const u32x4* el4 = reinterpret_cast<const u32x4*>(elbuf);
+  const u32x4* pw4 = reinterpret_cast<const u32x4*>(pw);
 #define DCKV_VALUE(NT, RGT) \
-  launch_value<NT, RGT>(p, sh, pool, num_pages, page_table, max_pages, seq_lens, pb4, el4, vpart, vel, stream)
+  launch_value<NT, RGT>(p, sh, pool, num_pages, page_table, max_pages, seq_lens, pw4, vpart, vel, stream)
   if (p.pass.n_slices > 1)
-    e = launch_value_shared(p, sh, pool, num_pages, page_table, max_pages, seq_lens, pb4, el4, vpart,
-                            vel, stream);
+    e = launch_value_shared(p, sh, pool, num_pages, page_table, max_pages, seq_lens, pw4, vpart, vel,
+                            stream);
   else if (p.pass.nt == 1)
     e = sh.rgt == 8 ? DCKV_VALUE(1, 8) : sh.rgt == 6 ? DCKV_VALUE(1, 6) : DCKV_VALUE(1, 4);
   else

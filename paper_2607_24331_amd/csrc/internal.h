@@ -30,6 +30,8 @@ struct HeadTables {
 
 constexpr int kMaxSlices = 8;     // (query, head) row slices of the MFMA decode path
 constexpr int kSliceHeads = 32;   // at most two 16-head MFMA tiles per slice
+constexpr int kUnitPages = 8;     // pages of a two-pass score work-group (one softmax exponent)
+constexpr int kSharedWaves = 8;   // waves of a value work-group walking pages together (several slices)
 
 // Schedule of the MFMA decode path (bf16 latents), fixed by the plan.  Rows
 // (query, head) are ordered by (group, head, query), with the groups taken
@@ -92,15 +94,16 @@ struct DecodeShape {
   int32_t chunk_pages;      // pages a value chunk
   int32_t n_chunks;         // value chunks a sequence
   int32_t rgt;              // 16-rank value tiles a value work-group (4, 6 or 8), or with
-                            // several row slices a wave (1, 2 or 4; eight waves a work-group)
-  int32_t n_rgroups;        // value rank groups: ceil(r_v / (16 rgt)), with slices ceil(r_v / (128 rgt))
+                            // several row slices a wave (kSharedWaves waves a work-group)
+  int32_t n_rgroups;        // value rank groups: ceil(r_v / (16 rgt)), with slices
+                            // ceil(r_v / (16 kSharedWaves rgt))
   size_t off_qt;            // workspace byte offsets
   size_t off_ml;            // (m, l) of splits; two-pass: (E, L) of chunks
   size_t off_acc;           // split accumulators; two-pass: chunk accumulators
   size_t off_opart;         // merged value-latent rows
   size_t off_rt;            // rotary decode: transposed key factors
-  size_t off_p;             // softmax weights (bf16): rotary splits; two-pass pages
-  size_t off_el;            // two-pass: per-page (e, l) records
+  size_t off_p;             // softmax weights (bf16): rotary splits; two-pass pages (with
+                            // their (e, l) records)
   size_t bytes;
 };
 

@@ -495,7 +495,7 @@ int dckv_decode_launch_info(const dckv_plan* p, int32_t batch, int32_t max_conte
   info->split_tokens = sh.split_tokens;
   info->n_split = sh.n_split;
   info->head_slices = sh.pass ? p->pass.n_slices : (sh.mfma ? p->mfma.n_slices : 1);
-  info->value_tiles = sh.pass ? (p->pass.n_slices > 1 ? 8 * sh.rgt : sh.rgt) : 0;
+  info->value_tiles = sh.pass ? (p->pass.n_slices > 1 ? dckv::kSharedWaves * sh.rgt : sh.rgt) : 0;
   return DCKV_OK;
 }
 
