@@ -997,6 +997,155 @@ __global__ __launch_bounds__(256) void upproj_rows(const float* __restrict__ ame
   }
 }
 
+// ---------------------------------------------------------------------------
+// Up-projection on MFMA: o[row][c] = sum_r a[row][r] R_v[r][kv d_h + c] for
+// the rows of one KV head (sequence, query, head of the KV head).  Grid
+// (column tiles of CT, KV heads, groups of 64 rows), four waves.  The
+// work-group's R_v block (r_v x CT bf16) is loaded once, in 8 x 8 units
+// transposed in registers, and stored in LDS rank-contiguous per column:
+// the MFMA's B operand takes 8 consecutive ranks of one column a lane.  The
+// waves are the row group's 16-row tiles (1, 2 or 4) times KS = 4 / tiles
+// rank ranges; a wave's A operand is its 16 merged rows (fp32 split into
+// bf16 hi + lo parts) read from global memory in operand order, KA rank
+// steps ahead.  The rank ranges' sums are added through LDS in a fixed
+// order.
+template <int CT>
+__global__ __launch_bounds__(256) void upproj_mfma(const float* __restrict__ amerged,
+                                                   const bf16* __restrict__ Rv,
+                                                   float* __restrict__ out, int rows, int rv,
+                                                   HeadTables tb) {
+  constexpr int NC = CT / 16;                  // column tiles of a wave
+  constexpr int KA = 4;                        // rank steps of A loads in flight
+  constexpr int UB = 2;                        // R_v units (8 x 8) a thread a batch
+  extern __shared__ __align__(16) unsigned char smem[];
+  bf16* rt = reinterpret_cast<bf16*>(smem);    // [CT][stride]
+  const int ctile = blockIdx.x, kv = blockIdx.y, row0 = blockIdx.z * 64;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int lr = lane & 15, lq = lane >> 4;
+  const int dh = tb.head_dim, n = tb.n_kv_heads * dh, qpk = tb.q_per_kv;
+  const int nrow = min(64, rows - row0);
+  const int tiles = nrow <= 16 ? 1 : (nrow <= 32 ? 2 : 4);
+  const int KS = 4 / tiles;
+  const int mt = w % tiles, ks = w / tiles;
+  const int nstep = (rv + 31) >> 5;            // 32-rank steps
+  const int stride = 32 * nstep + 8;           // LDS row of one column (elements)
+  const int col0 = kv * dh + ctile * CT;
+
+  // this lane's A row (clamped; results of rows past the end are dropped)
+  const int lrow = row0 + 16 * mt + lr;
+  const int crow = min(lrow, rows - 1);
+  const float* arow = amerged + (int64_t(crow / qpk) * tb.n_q_heads + kv * qpk + crow % qpk) * rv;
+  const int s0 = ks * nstep / KS, s1 = (ks + 1) * nstep / KS;   // this wave's rank steps
+  float4 av[KA][2];
+  auto aload = [&](int st, float4 (&d)[2]) {   // ranks 32 st + 8 lq .. +7, zero past r_v
+    const int r = 32 * min(st, nstep - 1) + 8 * lq;
+    if ((rv & 3) == 0 && r + 8 <= rv) {          // 16-byte aligned rows
+      d[0] = *reinterpret_cast<const float4*>(arow + r);
+      d[1] = *reinterpret_cast<const float4*>(arow + r + 4);
+    } else {
+      float t[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) t[j] = r + j < rv ? arow[r + j] : 0.f;
+      d[0] = make_float4(t[0], t[1], t[2], t[3]);
+      d[1] = make_float4(t[4], t[5], t[6], t[7]);
+    }
+  };
+#pragma unroll
+  for (int k = 0; k < KA; ++k) aload(s0 + k, av[k]);
+
+  // the R_v block in units of 8 ranks x 8 columns (unit u: ranks 8 (u / (CT
+  // / 8)) .., columns 8 (u % (CT / 8)) ..), UB units a thread a batch: eight
+  // 16-byte row loads, transposed in registers into eight rank-contiguous
+  // 16-byte column pieces; ranks past r_v are stored as zero
+  const int nunit = 4 * nstep * (CT / 8);
+  for (int base = 0; base < nunit; base += 256 * UB) {
+    u32x4 v[UB][8];
+#pragma unroll
+    for (int k = 0; k < UB; ++k) {
+      const int u = min(base + tid + 256 * k, nunit - 1);
+      const int r0 = 8 * (u / (CT / 8)), c8 = 8 * (u % (CT / 8));
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        v[k][i] = *reinterpret_cast<const u32x4*>(Rv + int64_t(min(r0 + i, rv - 1)) * n + col0 + c8);
+    }
+#pragma unroll
+    for (int k = 0; k < UB; ++k) {
+      const int u = base + tid + 256 * k;
+      if (u < nunit) {
+        const int r0 = 8 * (u / (CT / 8)), c8 = 8 * (u % (CT / 8));
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          if (r0 + i >= rv) v[k][i] = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          u32x4 t;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const uint32_t a = v[k][2 * j][c >> 1], b = v[k][2 * j + 1][c >> 1];
+            t[j] = (c & 1) ? ((a >> 16) | (b & 0xFFFF0000u)) : ((a & 0xFFFFu) | (b << 16));
+          }
+          *reinterpret_cast<u32x4*>(rt + (c8 + c) * stride + r0) = t;
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  floatx4 acc[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) acc[c] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int sb = s0; sb < s1; sb += KA) {
+#pragma unroll
+    for (int k = 0; k < KA; ++k) {
+      const int st = sb + k;
+      if (st < s1) {
+        const float f[8] = {av[k][0].x, av[k][0].y, av[k][0].z, av[k][0].w,
+                            av[k][1].x, av[k][1].y, av[k][1].z, av[k][1].w};
+        aload(st + KA, av[k]);
+        u32x4 hi, lo;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const bf16 h0 = static_cast<bf16>(f[2 * j]), h1 = static_cast<bf16>(f[2 * j + 1]);
+          const bf16 l0 = static_cast<bf16>(f[2 * j] - static_cast<float>(h0));
+          const bf16 l1 = static_cast<bf16>(f[2 * j + 1] - static_cast<float>(h1));
+          hi[j] = uint32_t(__builtin_bit_cast(uint16_t, h0)) | (uint32_t(__builtin_bit_cast(uint16_t, h1)) << 16);
+          lo[j] = uint32_t(__builtin_bit_cast(uint16_t, l0)) | (uint32_t(__builtin_bit_cast(uint16_t, l1)) << 16);
+        }
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+          const u32x4 B = *reinterpret_cast<const u32x4*>(rt + (16 * c + lr) * stride + 32 * st + 8 * lq);
+          acc[c] = mfma(hi, B, acc[c]);
+          acc[c] = mfma(lo, B, acc[c]);
+        }
+      }
+    }
+  }
+
+  // rank ranges ks > 0 -> LDS; ks = 0 adds them in ascending order and stores
+  __syncthreads();                             // the R_v block is no longer read
+  floatx4* red = reinterpret_cast<floatx4*>(smem);   // [wave][NC][64]
+  if (ks > 0) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c) red[(w * NC + c) * 64 + lane] = acc[c];
+  }
+  __syncthreads();
+  if (ks > 0) return;
+  for (int k2 = 1; k2 < KS; ++k2) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c) acc[c] += red[((k2 * tiles + mt) * NC + c) * 64 + lane];
+  }
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int row = row0 + 16 * mt + 4 * lq + v;
+    if (row < rows) {
+      const int bb = row / qpk, h = kv * qpk + row % qpk;
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+        out[(int64_t(bb) * tb.n_q_heads + h) * dh + ctile * CT + 16 * c + lr] = acc[c][v];
+    }
+  }
+}
+
 }  // namespace
 
 size_t pass_score_lds_bytes(const dckv_plan& p) {
@@ -1118,10 +1267,34 @@ hipError_t launch_score(const dckv_plan& p, const DecodeShape& sh, const u32x4* 
   return hipErrorInvalidValue;
 }
 
+size_t upproj_mfma_lds_bytes(const dckv_plan& p, int ct) {
+  const size_t stride = size_t((p.rv + 31) / 32) * 32 + 8;
+  return std::max<size_t>(size_t(ct) * stride * 2, size_t(4) * (ct / 16) * 64 * 16);
+}
+
 hipError_t launch_upproj(const dckv_plan& p, int32_t batch_rows, const float* amerged,
                          const void* R_value, float* out, hipStream_t stream) {
+  const int rows = batch_rows * p.qpk;          // rows a KV head
+  // MFMA for at least 8 rows a KV head (fewer: R_v is read once either way
+  // and the VALU kernel reads it straight into registers): 32-column tiles
+  // while the transposed R_v block fits LDS and the grid still fills the
+  // chip, else 16
+  const int groups = p.Hkv * ((rows + 63) / 64);
+  const bool fit32 = p.dh % 32 == 0 && upproj_mfma_lds_bytes(p, 32) <= 160 * 1024;
+  const bool fit16 = p.dh % 16 == 0 && upproj_mfma_lds_bytes(p, 16) <= 160 * 1024;
+  const int ctm = rows < 8 ? 0
+                  : (fit32 && (groups * (p.dh / 32) >= 256 || !fit16)) ? 32 : (fit16 ? 16 : 0);
+  if (ctm) {
+    const size_t lds = upproj_mfma_lds_bytes(p, ctm);
+    auto kern = ctm == 32 ? upproj_mfma<32> : upproj_mfma<16>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3(p.dh / ctm, p.Hkv, (rows + 63) / 64), dim3(256), lds, stream,
+                       amerged, static_cast<const bf16*>(R_value), out, rows, p.rv, p.tables);
+    return hipGetLastError();
+  }
   // column tiles of 16 when tiles of 32 would leave most compute units idle
-  const int rows = batch_rows * p.qpk;
   const int rblocks = (rows + 7) / 8;
   const int ct = int64_t(rblocks) * p.Hkv * ((p.dh + 31) / 32) >= 256 ? 32 : 16;
   const size_t lds = upproj_lds_bytes(p, ct);
