@@ -241,6 +241,17 @@ KERNEL_SOURCES = ("paper_2607_24331_amd/csrc/decode_mfma.hip", "paper_2607_24331
                   "paper_2607_24331_amd/csrc/internal.h")
 ROPE_KERNEL_SOURCES = ("paper_2607_24331_amd/csrc/rope.hip", "paper_2607_24331_amd/csrc/plan.cpp",
                        "paper_2607_24331_amd/csrc/internal.h")
+PASS_KERNEL_SOURCES = ("paper_2607_24331_amd/csrc/decode_pass.hip", "paper_2607_24331_amd/csrc/plan.cpp",
+                       "paper_2607_24331_amd/csrc/internal.h")
+
+
+def sources_of(kernel):
+    """The sources whose hash a counter summary of `kernel` is tied to."""
+    if kernel == "rope_scores":
+        return ROPE_KERNEL_SOURCES
+    if kernel in ("value_pages", "value_shared", "score_pages"):
+        return PASS_KERNEL_SOURCES
+    return KERNEL_SOURCES
 
 
 def kernel_sources_sha256(sources=KERNEL_SOURCES):
@@ -263,7 +274,7 @@ def measured_traffic(wl, launch, Q=1, kernel="split_mfma"):
     root = os.path.dirname(os.path.abspath(__file__))
     tag = wl.name if Q == 1 else f"{wl.name}_q{Q}"
     path = os.path.join(root, "profiles", f"{kernel}_{tag}_counters.md")
-    sources = ROPE_KERNEL_SOURCES if kernel == "rope_scores" else KERNEL_SOURCES
+    sources = sources_of(kernel)
     if not os.path.exists(path):
         return None
     keys = {}
