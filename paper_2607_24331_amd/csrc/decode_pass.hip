@@ -563,6 +563,10 @@ __global__ __launch_bounds__(W * 64, 1) void value_shared(
     int64_t value_base, int RT, const u32x4* __restrict__ pw, float* __restrict__ vpart,
     float* __restrict__ vel) {
   constexpr int NTH = W * 64;
+  // launched with RT = RTMAX only (the plan's row-tile count picks the
+  // instantiation); the check also lets the compiler take the count as
+  // fixed, which keeps the page loop free of spills
+  if (RT != RTMAX) return;
   constexpr int IP = 2 * RGTW;                      // value loads a page a wave
   constexpr int SV = (RTMAX * 160 + NTH - 1) / NTH; // staged 16-byte loads a thread a page
   extern __shared__ __align__(16) unsigned char smem[];
@@ -1223,18 +1227,28 @@ hipError_t launch_shared(const dckv_plan& p, const DecodeShape& sh, const void* 
   return hipGetLastError();
 }
 
-// The shared-weights value pass: RGTW (sh.rgt) value tiles a wave, for up
-// to 8 or 16 row tiles.
+// The shared-weights value pass for the plan's RT = 2J row tiles (J >= 2
+// slices of two tiles), RGTW = sh.rgt value tiles a wave; each row-tile
+// count has its own instantiation.
 hipError_t launch_value_shared(const dckv_plan& p, const DecodeShape& sh, const void* pool,
                                int64_t num_pages, const int32_t* page_table, int32_t max_pages,
                                const int32_t* seq_lens, const u32x4* pw, float* vpart,
                                float* vel, hipStream_t stream) {
   const int RT = p.pass.n_slices * p.pass.nt;
-#define DCKV_SHARED(RTMAX, RGTW, DP) \
-  launch_shared<kSharedWaves, RTMAX, RGTW, DP>(p, sh, pool, num_pages, page_table, max_pages, seq_lens, pw, vpart, vel, stream)
-  if (RT <= 8) return sh.rgt == 2 ? DCKV_SHARED(8, 2, 2) : DCKV_SHARED(8, 1, 8);
-  return DCKV_SHARED(16, 1, 4);
+#define DCKV_SHARED(RTC, RGTW, DP) \
+  launch_shared<kSharedWaves, RTC, RGTW, DP>(p, sh, pool, num_pages, page_table, max_pages, seq_lens, pw, vpart, vel, stream)
+  // the deepest ring of each shape that the compiler keeps out of scratch
+  switch (RT) {
+    case 4: return sh.rgt == 2 ? DCKV_SHARED(4, 2, 3) : DCKV_SHARED(4, 1, 4);
+    case 6: return sh.rgt == 2 ? DCKV_SHARED(6, 2, 2) : DCKV_SHARED(6, 1, 4);
+    case 8: return sh.rgt == 2 ? DCKV_SHARED(8, 2, 4) : DCKV_SHARED(8, 1, 8);
+    case 10: return DCKV_SHARED(10, 1, 6);
+    case 12: return DCKV_SHARED(12, 1, 4);
+    case 14: return DCKV_SHARED(14, 1, 3);
+    case 16: return DCKV_SHARED(16, 1, 3);
+  }
 #undef DCKV_SHARED
+  return hipErrorInvalidValue;
 }
 
 template <int NT, int RING>

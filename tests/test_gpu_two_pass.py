@@ -152,10 +152,12 @@ def test_two_pass_large_value_rank(rv):
 
 # (case, Q): several causal queries a sequence on the two-pass kernels.  Up
 # to 32 rows take one slice (the per-wave value pass); beyond, 2 to 8 slices
-# of up to 32 rows each share one walk over the value latents (4, 6, 8 and 16
-# row tiles); mha_odd holds a one-token and an empty sequence.
+# of up to 32 rows each share one walk over the value latents (4, 6, 8, 10,
+# 12, 14 and 16 row tiles, each its own kernel instance); mha_odd holds a
+# one-token and an empty sequence.
 MULTI_PASS = [("singletons", 3), ("gqa_uneven", 4), ("mha_odd", 8), ("mha32_two_tiles", 2),
-              ("mha32_two_tiles", 3), ("gqa_reordered", 4), ("mha32_two_tiles", 8)]
+              ("mha32_two_tiles", 3), ("gqa_reordered", 4), ("mha32_two_tiles", 5),
+              ("mha32_two_tiles", 6), ("mha32_two_tiles", 7), ("mha32_two_tiles", 8)]
 
 
 def _multi_plan(wl, Q, split=0, passes=2):
