@@ -1002,6 +1002,112 @@ __global__ __launch_bounds__(256) void upproj_rows(const float* __restrict__ ame
 }
 
 // ---------------------------------------------------------------------------
+// Up-projection for the few rows (at most RB) of one KV head, a product of
+// those rows with the head's r_v x d_h block of R_v that reads each of the
+// block's rank rows as whole 128-byte pieces.  Grid (64-column tiles, KV
+// heads), sixteen waves.  Lane: columns 8 (lane % 8) .. +7 of the tile, rank
+// group g = 8 w + lane / 8 of 128 (ranks g, g + 128, ...), sixteen 16-byte
+// R_v loads in flight.  The merged rows are staged in LDS first.  Fixed
+// order of the sums: each lane sums its ranks in ascending order, a wave's
+// eight rank groups are added by xor shuffles over lane bits 3, 4 and 5, and
+// the sixteen waves' sums are added in wave order.
+template <int RB>
+__global__ __launch_bounds__(1024) void upproj_wide(const float* __restrict__ amerged,
+                                                    const bf16* __restrict__ Rv,
+                                                    float* __restrict__ out, int rows, int rv,
+                                                    HeadTables tb) {
+  constexpr int U = 16;                        // R_v loads a batch
+  constexpr int RG = 128;                      // rank groups
+  const int ct = blockIdx.x, kv = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int c8 = lane & 7, rg = 8 * w + (lane >> 3);
+  const int dh = tb.head_dim, n = tb.n_kv_heads * dh, qpk = tb.q_per_kv;
+  extern __shared__ float sa[];                // [rows][rv]; later [16 waves][RB * 64]
+  const bf16* src = Rv + (int64_t(kv) * dh + ct * 64);   // uniform base; lane offsets below
+  u32x4 v[U];
+  auto issue = [&](int rbase) {
+#pragma unroll
+    for (int k = 0; k < U; ++k)
+      v[k] = *reinterpret_cast<const u32x4*>(src + (min(rbase + RG * k, rv - 1) * n + 8 * c8));
+  };
+  auto arow = [&](int q) {                     // merged row of local row q
+    return amerged + (int64_t(q / qpk) * tb.n_q_heads + kv * qpk + q % qpk) * rv;
+  };
+  issue(rg);                                   // the first batch travels with the staging
+  if ((rv & 3) == 0) {
+    const int rv4 = rv >> 2, nvec = rows * rv4;
+    for (int i0 = tid; i0 < nvec; i0 += 2048) {   // two loads in flight
+      const int i1 = min(i0 + 1024, nvec - 1);
+      const float4 s0 = reinterpret_cast<const float4*>(arow(i0 / rv4))[i0 % rv4];
+      const float4 s1 = reinterpret_cast<const float4*>(arow(i1 / rv4))[i1 % rv4];
+      reinterpret_cast<float4*>(sa)[i0] = s0;
+      if (i0 + 1024 < nvec) reinterpret_cast<float4*>(sa)[i0 + 1024] = s1;
+    }
+  } else {
+    for (int i = tid; i < rows * rv; i += 1024) sa[i] = arow(i / rv)[i % rv];
+  }
+  __syncthreads();
+  float acc[RB][8];
+#pragma unroll
+  for (int q = 0; q < RB; ++q)
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) acc[q][jj] = 0.f;
+  // one batch covers 128 U ranks (all of r_v = 2048 at U = 16)
+  for (int r = rg; r < rv; r += RG * U) {
+    if (r != rg) issue(r);
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int rr = r + RG * k;
+      if (rr < rv) {
+        float f[8];
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          f[2 * jj] = __uint_as_float(v[k][jj] << 16);
+          f[2 * jj + 1] = __uint_as_float(v[k][jj] & 0xFFFF0000u);
+        }
+#pragma unroll
+        for (int q = 0; q < RB; ++q) {
+          if (q < rows) {
+            const float aq = sa[q * rv + rr];
+#pragma unroll
+            for (int jj = 0; jj < 8; ++jj) acc[q][jj] = fmaf(aq, f[jj], acc[q][jj]);
+          }
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < RB; ++q)
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) {
+      float x = acc[q][jj];
+      x += __shfl_xor(x, 8);
+      x += __shfl_xor(x, 16);
+      x += __shfl_xor(x, 32);
+      acc[q][jj] = x;
+    }
+  __syncthreads();                             // the staged rows are read; their space is reused
+  float* red = sa;
+  if (lane < 8) {
+#pragma unroll
+    for (int q = 0; q < RB; ++q)
+      if (q < rows) {
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) red[w * (RB * 64) + q * 64 + 8 * c8 + jj] = acc[q][jj];
+      }
+  }
+  __syncthreads();
+  if (tid < rows * 64) {
+    const int q = tid >> 6, cc = tid & 63;
+    float t = 0.f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) t += red[k * (RB * 64) + tid];
+    const int bb = q / qpk, h = kv * qpk + q % qpk;
+    out[(int64_t(bb) * tb.n_q_heads + h) * dh + ct * 64 + cc] = t;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Up-projection on MFMA: o[row][c] = sum_r a[row][r] R_v[r][kv d_h + c] for
 // the rows of one KV head (sequence, query, head of the KV head).  Grid
 // (column tiles of CT, KV heads, groups of 64 rows), four waves.  The
@@ -1286,9 +1392,29 @@ size_t upproj_mfma_lds_bytes(const dckv_plan& p, int ct) {
   return std::max<size_t>(size_t(ct) * stride * 2, size_t(4) * (ct / 16) * 64 * 16);
 }
 
+size_t upproj_wide_lds_bytes(const dckv_plan& p, int rows, int rb) {
+  return std::max<size_t>(size_t(rows) * p.rv, size_t(16) * rb * 64) * 4;
+}
+
 hipError_t launch_upproj(const dckv_plan& p, int32_t batch_rows, const float* amerged,
                          const void* R_value, float* out, hipStream_t stream) {
   const int rows = batch_rows * p.qpk;          // rows a KV head
+  // at most 4 rows a KV head, with 64-column tiles that give the grid at
+  // least 32 work-groups: the wide kernel (whole 128-byte pieces of R_v;
+  // more rows would not fit its registers)
+  if (rows > 0 && rows <= 4 && p.dh % 64 == 0 && p.Hkv * (p.dh / 64) >= 32) {
+    const int rb = rows <= 1 ? 1 : (rows <= 2 ? 2 : 4);
+    const size_t lds = upproj_wide_lds_bytes(p, rows, rb);
+    if (lds <= 160 * 1024) {
+      auto kern = rb == 1 ? upproj_wide<1> : (rb == 2 ? upproj_wide<2> : upproj_wide<4>);
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(kern, dim3(p.dh / 64, p.Hkv), dim3(1024), lds, stream, amerged,
+                         static_cast<const bf16*>(R_value), out, rows, p.rv, p.tables);
+      return hipGetLastError();
+    }
+  }
   // MFMA for at least 8 rows a KV head (fewer: R_v is read once either way
   // and the VALU kernel reads it straight into registers): 32-column tiles
   // while the transposed R_v block fits LDS and the grid still fills the

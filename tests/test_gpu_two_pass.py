@@ -150,6 +150,25 @@ def test_two_pass_large_value_rank(rv):
         _check_all(wl, inp, out, f"rv{rv}/{'two-pass' if passes == 2 else 'single-pass'}")
 
 
+@pytest.mark.parametrize("rv, lens", [(250, (129,)), (2048, (70, 1, 300)), (333, (64, 65))])
+def test_few_rows_up_projection(rv, lens):
+    # one to three rows a KV head over 32 KV heads: the up-projection that
+    # reads whole 128-byte pieces of R_v rows; value ranks that are not a
+    # multiple of 4 (element-wise staging of the merged rows) or of 128
+    wl = custom_workload(name=f"few{rv}", seed=rv + len(lens), hidden=4096, num_q_heads=32,
+                         num_kv_heads=32, head_dim=128, group_of_kv=tuple(i // 8 for i in range(32)),
+                         group_rank=(96, 64, 160, 32), value_rank=rv, dtype="bf16",
+                         batch=len(lens), seq_lens=lens, prefill_lens=lens,
+                         factor_scheme="orthonormal")
+    inp = make_inputs(wl)
+    for passes in (2, 0):
+        plan = _plan(wl, 0, passes) if passes == 2 else _plan(wl, 0, 1)
+        print(f"[two-pass] few rows rv {rv} lens {lens} passes {passes}", flush=True)
+        pool = gpu_pool_with_append(inp, plan)
+        out = run_decode(inp, plan, pool)
+        _check_all(wl, inp, out, f"few-rows/rv{rv}/{'two-pass' if passes == 2 else 'single-pass'}")
+
+
 # (case, Q): several causal queries a sequence on the two-pass kernels.  Up
 # to 32 rows take one slice (the per-wave value pass); beyond, 2 to 8 slices
 # of up to 32 rows each share one walk over the value latents (4, 6, 8, 10,
