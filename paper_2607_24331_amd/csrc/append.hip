@@ -110,40 +110,39 @@ __global__ __launch_bounds__(256) void append_valu(const T* __restrict__ x, cons
 // sum_k x[token][k] * LT[column][k]: both operands are contiguous in k.
 // Work-group tile 128 tokens x 64 columns (so the long-context append of
 // 512 tokens x 3584 columns fills 224 of the 256 CUs).  k advances in
-// stages of 64.  Both tiles of a stage are staged through two LDS buffers
-// (rows padded to 72 elements so the 16 rows an MFMA operand load touches
-// fall in distinct banks) by loads that each cover 8 rows x 128 B, whole
-// cache lines: a load in MFMA operand order (16 rows x 64 B) halves the L1
-// throughput.  Every thread keeps the global loads of the next D stages in
-// flight.  Eight waves, two a SIMD (one wave alone cannot keep the matrix
-// pipe busy across the per-stage barrier): wave w owns tokens
-// 32 (w % 4) .. +31 against all 64 columns (2 x 4 tiles of 16 x 16) and the
-// k half w / 4 of every stage; at the end the upper k half's sums are added
-// to the lower half's through LDS (a fixed order).  Work-group ids that are
-// equal mod 8 run on one XCD; the id -> tile map gives each XCD a contiguous
-// run of tiles with the token tiles of one column tile adjacent, so that
-// column tile of L is fetched into the XCD's L2 once.  Rows past the token
-// count or the column space are clamped to valid rows and their results
-// discarded, so no load leaves its matrix.
+// stages of 64.  A stage (both tiles, 192 rows x 128 B) is copied from
+// global memory straight into LDS by the loads' LDS path (no registers, no
+// LDS store instructions): one wave instruction moves 8 rows x 128 B, whole
+// cache lines, to 1 KB of LDS in lane order, and the lane -> 16-byte piece
+// map is xor-swizzled by the row (LDS piece p of row r holds global piece
+// p ^ (r % 8)) so that the 16 rows an MFMA operand load touches fall in
+// distinct banks.  NB stage buffers: the loads run NB - 1 stages ahead, and
+// one barrier a stage (after the wave's own loads of that stage and its LDS
+// reads of the stage before have completed) both publishes the stage and
+// frees the buffer the next loads refill.  Eight waves, two a SIMD (one wave
+// alone cannot keep the matrix pipe busy across the per-stage barrier):
+// wave w owns tokens 32 (w % 4) .. +31 against all 64 columns (2 x 4 tiles
+// of 16 x 16) and the k half w / 4 of every stage; at the end the upper k
+// half's sums are added to the lower half's through LDS (a fixed order).
+// Work-group ids that are equal mod 8 run on one XCD; the id -> tile map
+// gives each XCD a contiguous run of tiles with the token tiles of one
+// column tile adjacent, so that column tile of L is fetched into the XCD's
+// L2 once.  Rows past the token count or the column space are clamped to
+// valid rows and their results discarded, so no load leaves its matrix.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kBM = 128;                  // tokens a work-group
 constexpr int kBN = 64;                   // columns a work-group
-constexpr int kBK = 64;                   // k a stage
+constexpr int kBK = 64;                   // k a stage (one 128-byte line a row)
 constexpr int kThreads = 512;
-constexpr int kLdsRow = kBK + 8;          // padded LDS row (elements)
-constexpr int kStageElems = (kBM + kBN) * kLdsRow;
-constexpr int kPieces = kBK / 8;                    // 16-byte pieces a row a stage
-constexpr int kRowsPerPass = kThreads / kPieces;      // rows one pass of all threads covers
-constexpr int kALoads = kBM / kRowsPerPass;          // 16-byte x loads a thread a stage
-constexpr int kBLoads = kBN / kRowsPerPass;          // 16-byte L loads a thread a stage
-constexpr int kStageBytes = 2 * kStageElems * 2;    // both buffers
+constexpr int kNB = 4;                    // LDS stage buffers
+constexpr int kBufBytes = (kBM + kBN) * kBK * 2;   // one stage: 24 blocks of 8 rows x 128 B
 constexpr int kExchBytes = 4 * 2 * 4 * 64 * 16;     // k-half exchange: 4 waves x 8 tiles x 64 lanes
-constexpr int kLdsBytes = kStageBytes > kExchBytes ? kStageBytes : kExchBytes;
+static_assert(kExchBytes <= kNB * kBufBytes, "the exchange fits the stage buffers");
 
-template <int D>
+template <int NB>
 __global__ __launch_bounds__(kThreads, 1) void append_mfma(const bf16* __restrict__ x,
                                                           const bf16* __restrict__ LkT,
                                                           const bf16* __restrict__ LvT,
@@ -153,8 +152,7 @@ __global__ __launch_bounds__(kThreads, 1) void append_mfma(const bf16* __restric
                                                           int64_t page_elems, int64_t value_base,
                                                           int64_t num_pages, int n_tok_tiles,
                                                           int n_tiles) {
-  __shared__ __align__(16) unsigned char smem[kLdsBytes];
-  bf16* lds = reinterpret_cast<bf16*>(smem);
+  __shared__ __align__(1024) unsigned char smem[NB * kBufBytes];
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 15, lq = lane >> 4;
@@ -170,37 +168,37 @@ __global__ __launch_bounds__(kThreads, 1) void append_mfma(const bf16* __restric
   const int wm = 32 * (w & 3);                        // this wave's first token
   const int kh = w >> 2;                              // this wave's k half
 
-  // staging: rows prow + kRowsPerPass i of both tiles, 16-byte piece
-  // tid % kPieces (a wave covers 8 rows x 128 B)
-  const int piece = tid % kPieces, prow = tid / kPieces;
-  const bf16* ga[kALoads];
+  // loads: wave w fills 8-row blocks 3w .. 3w + 2 of a stage (16 x blocks,
+  // then 8 L blocks); lane: row lane / 8 of its block, LDS piece lane % 8,
+  // which holds global piece (lane % 8) ^ (row % 8)
+  const int lrow = lane >> 3, gpiece = (lane & 7) ^ lrow;
+  const bf16* gsrc[3];
+  int loff[3];
 #pragma unroll
-  for (int i = 0; i < kALoads; ++i) {
-    const int t = min(tok0 + prow + kRowsPerPass * i, n_tok - 1);
-    ga[i] = x + int64_t(t) * m + 8 * piece;
-  }
-  const bf16* gb[kBLoads];
-#pragma unroll
-  for (int i = 0; i < kBLoads; ++i) {
-    const int c = col0 + prow + kRowsPerPass * i;
+  for (int j = 0; j < 3; ++j) {
+    const int blk = 3 * w + j;
+    loff[j] = blk * 1024;
     const bf16* r;
-    if (c < RK)
-      r = LkT + int64_t(c) * m;
-    else if (c < RKp)
-      r = LkT;                                // padding column: written as zero below
-    else
-      r = LvT + int64_t(min(c - RKp, rv - 1)) * m;
-    gb[i] = r + 8 * piece;
+    if (blk < 16) {
+      const int t = min(tok0 + 8 * blk + lrow, n_tok - 1);
+      r = x + int64_t(t) * m;
+    } else {
+      const int c = col0 + 8 * (blk - 16) + lrow;
+      if (c < RK)
+        r = LkT + int64_t(c) * m;
+      else if (c < RKp)
+        r = LkT;                                // padding column: written as zero below
+      else
+        r = LvT + int64_t(min(c - RKp, rv - 1)) * m;
+    }
+    gsrc[j] = r + 8 * gpiece;
   }
-  u32x4_t ra[D][kALoads], rb[D][kBLoads];
   const int nst = m / kBK;
-  auto kof = [&](int st) { return min(st, nst - 1) * kBK; };   // past the end: re-read the last
-  auto gload = [&](u32x4_t (&a)[kALoads], u32x4_t (&b)[kBLoads], int st) {
-    const int k = kof(st);
+  auto issue = [&](int st, unsigned char* buf) {      // past the end: re-read the last stage
+    const int k = min(st, nst - 1) * kBK;
 #pragma unroll
-    for (int i = 0; i < kALoads; ++i) a[i] = *reinterpret_cast<const u32x4_t*>(ga[i] + k);
-#pragma unroll
-    for (int i = 0; i < kBLoads; ++i) b[i] = *reinterpret_cast<const u32x4_t*>(gb[i] + k);
+    for (int j = 0; j < 3; ++j)
+      __builtin_amdgcn_global_load_lds(gsrc[j] + k, buf + loff[j], 16, 0, 0);
   };
 
   floatx4_t acc[2][4];
@@ -209,52 +207,53 @@ __global__ __launch_bounds__(kThreads, 1) void append_mfma(const bf16* __restric
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
-  // keep the prologue's stages in ring order, so that waiting for the
-  // oldest stage never waits for the younger ones (vmcnt counts in order)
+  const int kp = 4 * kh + lq;                         // this lane's 16-byte k piece
+  auto stage = [&](int st, unsigned char* cur, unsigned char* nxt) {
+    // wait until this wave's loads of stage st (the oldest of the NB - 1
+    // stages in flight, three loads each) and its LDS reads of the previous
+    // stage are done, then meet the other waves; the asm is a compiler
+    // barrier too, so no LDS access moves across it
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"i"(3 * (NB - 2)) : "memory");
+    issue(st + NB - 1, nxt);
+    u32x4_t a[2], b[4];
 #pragma unroll
-  for (int d = 0; d < D; ++d) {
-    gload(ra[d], rb[d], d);
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  // nst is a multiple of D (the launcher picks D so), and D is even or 1
-  for (int st0 = 0; st0 < nst; st0 += D) {
+    for (int i = 0; i < 2; ++i) {
+      const int row = wm + 16 * i + lr;
+      a[i] = *reinterpret_cast<const u32x4_t*>(cur + row * 128 + 16 * (kp ^ (row & 7)));
+    }
 #pragma unroll
-    for (int d = 0; d < D; ++d) {
-      const int buf = (D == 1) ? (st0 & 1) : (d & 1);
-      bf16* A = lds + buf * kStageElems;
-      bf16* B = A + kBM * kLdsRow;
+    for (int j = 0; j < 4; ++j) {
+      const int row = 16 * j + lr;
+      b[j] = *reinterpret_cast<const u32x4_t*>(cur + 16 * 1024 + row * 128 + 16 * (kp ^ (row & 7)));
+    }
 #pragma unroll
-      for (int i = 0; i < kALoads; ++i)
-        *reinterpret_cast<u32x4_t*>(A + (prow + kRowsPerPass * i) * kLdsRow + 8 * piece) = ra[d][i];
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int i = 0; i < kBLoads; ++i)
-        *reinterpret_cast<u32x4_t*>(B + (prow + kRowsPerPass * i) * kLdsRow + 8 * piece) = rb[d][i];
-      gload(ra[d], rb[d], st0 + d + D);
-      __syncthreads();
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a[i]),
+                                                            __builtin_bit_cast(bf16x8_t, b[j]),
+                                                            acc[i][j], 0, 0, 0);
+  };
 #pragma unroll
-      for (int ks = 0; ks < kBK / 64; ++ks) {
-        const int kk = (kBK / 2) * kh + 32 * ks + 8 * lq;   // this wave's k half, step ks
-        u32x4_t a[2], b[4];
+  for (int u = 0; u < NB - 1; ++u) issue(u, smem + u * kBufBytes);
+  if (nst % NB == 0) {
+    for (int st0 = 0; st0 < nst; st0 += NB) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
-          a[i] = *reinterpret_cast<const u32x4_t*>(A + (wm + 16 * i + lr) * kLdsRow + kk);
+      for (int u = 0; u < NB; ++u)
+        stage(st0 + u, smem + u * kBufBytes, smem + ((u + NB - 1) % NB) * kBufBytes);
+    }
+  } else {
+    for (int st0 = 0; st0 < nst; st0 += NB) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          b[j] = *reinterpret_cast<const u32x4_t*>(B + (16 * j + lr) * kLdsRow + kk);
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a[i]),
-                                                                __builtin_bit_cast(bf16x8_t, b[j]),
-                                                                acc[i][j], 0, 0, 0);
-      }
+      for (int u = 0; u < NB; ++u)
+        if (st0 + u < nst) stage(st0 + u, smem + u * kBufBytes, smem + ((u + NB - 1) % NB) * kBufBytes);
     }
   }
+  __builtin_amdgcn_s_waitcnt(0);                      // the re-reads past the end have landed
 
   // upper k half -> LDS, lower half adds it (lane-private slots, same order everywhere)
   floatx4_t* ex = reinterpret_cast<floatx4_t*>(smem);   // [4 waves][8 tiles][64 lanes]
-  __syncthreads();                                       // staging buffers no longer read
+  __syncthreads();                                       // stage buffers no longer read
   if (kh == 1) {
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -296,14 +295,14 @@ __global__ __launch_bounds__(kThreads, 1) void append_mfma(const bf16* __restric
   }
 }
 
-template <int D>
+template <int NB>
 hipError_t launch_append_mfma(const dckv_plan& p, const void* x, int32_t n_tok, const void* Lk,
                               const void* Lv, const int64_t* slot, void* pool, int64_t num_pages,
                               hipStream_t stream) {
   const int ncols = p.RKp + p.rv;
   const int n_tok_tiles = (n_tok + kBM - 1) / kBM;
   const int n_tiles = n_tok_tiles * ((ncols + kBN - 1) / kBN);
-  hipLaunchKernelGGL(append_mfma<D>, dim3(n_tiles), dim3(kThreads), 0, stream,
+  hipLaunchKernelGGL(append_mfma<NB>, dim3(n_tiles), dim3(kThreads), 0, stream,
                      static_cast<const bf16*>(x), static_cast<const bf16*>(Lk),
                      static_cast<const bf16*>(Lv), slot, static_cast<bf16*>(pool), n_tok, p.m,
                      p.RK, p.RKp, p.rv, p.page_elems, p.value_base, num_pages, n_tok_tiles, n_tiles);
@@ -330,14 +329,8 @@ hipError_t launch_append(const dckv_plan& p, const void* x, int32_t n_tok, const
                          hipStream_t stream) {
   if (p.dtype == DCKV_F32)
     return launch_append_t<float>(p, x, n_tok, L_keys, L_value, slot, pool, num_pages, stream);
-  if (p.m % kBK == 0) {
-    const int nst = p.m / kBK;
-    if (nst % 4 == 0)
-      return launch_append_mfma<4>(p, x, n_tok, L_keys, L_value, slot, pool, num_pages, stream);
-    if (nst % 2 == 0)
-      return launch_append_mfma<2>(p, x, n_tok, L_keys, L_value, slot, pool, num_pages, stream);
-    return launch_append_mfma<1>(p, x, n_tok, L_keys, L_value, slot, pool, num_pages, stream);
-  }
+  if (p.m % kBK == 0)
+    return launch_append_mfma<kNB>(p, x, n_tok, L_keys, L_value, slot, pool, num_pages, stream);
   return launch_append_t<bf16>(p, x, n_tok, L_keys, L_value, slot, pool, num_pages, stream);
 }
 
