@@ -150,6 +150,111 @@ __global__ __launch_bounds__(64) void fold_blocks(const float* __restrict__ q,
   }
 }
 
+// fold_mfma: the same blocks as fold_blocks, as one small product a (slice,
+// slot, 32-column chunk): the batch's query rows of the slot's head (B x d_h)
+// times the R rows of the chunk's columns (d_h x 32), on MFMA.  One wave;
+// its B operands (R, bf16) are loaded once and serve every 16-sequence tile
+// of the batch; the A operands are the fp32 query rows split into bf16 hi +
+// lo parts (two products a k step), accumulated in fp32.  Columns outside
+// the head's group latent, and slots without a head, are written as zero.
+// d_h a multiple of 32 (KS = d_h / 32 k steps).
+template <int KS>
+__global__ __launch_bounds__(64) void fold_mfma(const float* __restrict__ q,
+                                                const bf16* __restrict__ Rk,
+                                                u32x4* __restrict__ qblk_ws, int batch, float scale,
+                                                HeadTables tb, MfmaTables mt) {
+  const int J = mt.n_slices;
+  const int slice = blockIdx.x / 16, j = blockIdx.x % 16, pr = blockIdx.y;
+  const int nch0 = mt.kln[slice][0][0] + mt.kln[slice][0][1];
+  const int npairs = nch0 + (mt.nt > 1 ? mt.kln[slice][1][0] + mt.kln[slice][1][1] : 0);
+  if (pr >= npairs) return;
+  const int n = pr < nch0 ? 0 : 1;
+  const int ci = pr - (n ? nch0 : 0);
+  const int c = ci < mt.kln[slice][n][0] ? mt.kst[slice][n][0] + ci
+                                         : mt.kst[slice][n][1] + (ci - mt.kln[slice][n][0]);
+  const int row = mt.hord[slice][16 * n + j];           // query i * H_q + head h, or -1
+  const int h = row < 0 ? -1 : row % tb.n_q_heads, qi = row < 0 ? 0 : row / tb.n_q_heads;
+  const int lane = threadIdx.x, lr = lane & 15, lq = lane >> 4;
+  const int dh = tb.head_dim;
+  const int lo = h < 0 ? 0 : tb.koff_of_q[h], rk = h < 0 ? 0 : tb.rank_of_q[h];
+  // B operands: column 16 t + lr of the chunk, d = 32 ks + 8 lq .. +7
+  u32x4 bR[2][KS];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int k = 32 * c + 16 * t + lr;
+    const bool live = k >= lo && k < lo + rk;
+    const bf16* src = live ? Rk + tb.roff_of_q[h] + int64_t(k - lo) * tb.rstride_of_q[h] + tb.rcol_of_q[h]
+                           : Rk;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      bR[t][ks] = live ? load16(src + 32 * ks + 8 * lq) : u32x4{0u, 0u, 0u, 0u};
+  }
+  // output columns of this lane: 16 t + lr, t = 0, 1
+  bool out_live[2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int k = 32 * c + 16 * t + lr;
+    out_live[t] = k >= lo && k < lo + rk;
+  }
+  const int hq = h < 0 ? 0 : h;
+  float4 qa[KS][2], qn[KS][2];
+  auto qload = [&](float4 (&d)[KS][2], int b0) {      // this lane's A row (clamped)
+    const int ba = min(b0 + lr, batch - 1);
+    const float* qh = q + ((int64_t(ba) * tb.n_queries + qi) * tb.n_q_heads + hq) * dh + 8 * lq;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      d[ks][0] = *reinterpret_cast<const float4*>(qh + 32 * ks);
+      d[ks][1] = *reinterpret_cast<const float4*>(qh + 32 * ks + 4);
+    }
+  };
+  qload(qa, 0);
+  for (int b0 = 0; b0 < batch; b0 += 16) {
+    if (b0 + 16 < batch) qload(qn, b0 + 16);           // the next tile's rows in flight
+    floatx4 acc[2] = {floatx4{0.f, 0.f, 0.f, 0.f}, floatx4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const float f[8] = {qa[ks][0].x, qa[ks][0].y, qa[ks][0].z, qa[ks][0].w,
+                          qa[ks][1].x, qa[ks][1].y, qa[ks][1].z, qa[ks][1].w};
+      u32x4 ah, al;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bf16 h0 = static_cast<bf16>(f[2 * e]), h1 = static_cast<bf16>(f[2 * e + 1]);
+        const bf16 l0 = static_cast<bf16>(f[2 * e] - static_cast<float>(h0));
+        const bf16 l1 = static_cast<bf16>(f[2 * e + 1] - static_cast<float>(h1));
+        ah[e] = uint32_t(__builtin_bit_cast(uint16_t, h0)) | (uint32_t(__builtin_bit_cast(uint16_t, h1)) << 16);
+        al[e] = uint32_t(__builtin_bit_cast(uint16_t, l0)) | (uint32_t(__builtin_bit_cast(uint16_t, l1)) << 16);
+      }
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        acc[t] = mfma(ah, bR[t][ks], acc[t]);
+        acc[t] = mfma(al, bR[t][ks], acc[t]);
+      }
+    }
+    // lane holds sequences b0 + 4 lq + v of columns 16 t + lr
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int b = b0 + 4 * lq + v;
+      if (b >= batch) continue;
+      bf16* blk = reinterpret_cast<bf16*>(qblk_ws + (int64_t(b * J + slice) * mt.max_pairs + pr) * 128);
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int kk = 16 * t + lr;
+        const float x = out_live[t] ? acc[t][v] * scale : 0.f;
+        const bf16 vh = static_cast<bf16>(x);
+        const bf16 vl = static_cast<bf16>(x - static_cast<float>(vh));
+        const int l = 16 * (kk >> 3) + j, e = kk & 7;
+        blk[l * 8 + e] = vh;
+        blk[512 + l * 8 + e] = vl;
+      }
+    }
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      qa[ks][0] = qn[ks][0];
+      qa[ks][1] = qn[ks][1];
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // W waves (4 or 8) a work-group; NT 16-head tiles; at most MTW value M-tiles
 // (16 ranks) a wave; key ring blocks of KR loads, value ring blocks of VR
@@ -890,6 +995,15 @@ hipError_t launch_merge_upproj(const dckv_plan& p, const DecodeShape& sh, const 
 hipError_t launch_fold(const dckv_plan& p, const MfmaTables& mt, int32_t batch, const float* q,
                        const void* R_keys, void* qblk, hipStream_t stream) {
   const float scale = kLog2e / std::sqrt(float(p.dh));
+  // d_h 64 or 128: one wave a (slice, slot, chunk) for all sequences, on
+  // MFMA; other head sizes: one wave a (sequence, slice, slot, chunk)
+  if (p.dh == 64 || p.dh == 128) {
+    auto kern = p.dh == 64 ? fold_mfma<2> : fold_mfma<4>;
+    hipLaunchKernelGGL(kern, dim3(mt.n_slices * 16, mt.max_pairs), dim3(64), 0, stream, q,
+                       static_cast<const bf16*>(R_keys), static_cast<u32x4*>(qblk), batch, scale,
+                       p.tables, mt);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(fold_blocks, dim3(batch * mt.n_slices, 16, mt.max_pairs), dim3(64), 0, stream, q,
                      static_cast<const bf16*>(R_keys), static_cast<u32x4*>(qblk), scale, p.tables,
                      mt);

@@ -1109,9 +1109,9 @@ __global__ __launch_bounds__(1024) void upproj_wide(const float* __restrict__ am
 
 // ---------------------------------------------------------------------------
 // Up-projection on MFMA: o[row][c] = sum_r a[row][r] R_v[r][kv d_h + c] for
-// the rows of one KV head (sequence, query, head of the KV head).  Grid
-// (column tiles of CT, KV heads, groups of 64 rows), four waves.  The
-// work-group's R_v block (r_v x CT bf16) is loaded once, in 8 x 8 units
+// the rows of one KV head (sequence, query, head of the KV head).  One
+// work-group of four waves a (column tile of CT, KV head, group of 64
+// rows).  The work-group's R_v block (r_v x CT bf16) is loaded once, in 8 x 8 units
 // transposed in registers, and stored in LDS rank-contiguous per column:
 // the MFMA's B operand takes 8 consecutive ranks of one column a lane.  The
 // waves are the row group's 16-row tiles (1, 2 or 4) times KS = 4 / tiles
@@ -1129,7 +1129,14 @@ __global__ __launch_bounds__(256) void upproj_mfma(const float* __restrict__ ame
   constexpr int UB = 2;                        // R_v units (8 x 8) a thread a batch
   extern __shared__ __align__(16) unsigned char smem[];
   bf16* rt = reinterpret_cast<bf16*>(smem);    // [CT][stride]
-  const int ctile = blockIdx.x, kv = blockIdx.y, row0 = blockIdx.z * 64;
+  // 1-D grid, XCD-aware: work-group ids equal mod 8 run on one XCD, and all
+  // column tiles of one (KV head, row group) share an XCD, so its merged rows
+  // are fetched into that XCD's L2 once
+  const int nct = tb.head_dim / CT, ngr = tb.n_kv_heads * ((rows + 63) / 64);
+  const int xcd = blockIdx.x & 7, pos = blockIdx.x >> 3;
+  const int grp = 8 * (pos / nct) + xcd, ctile = pos % nct;
+  if (grp >= ngr) return;
+  const int kv = grp % tb.n_kv_heads, row0 = (grp / tb.n_kv_heads) * 64;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lq = lane >> 4;
   const int dh = tb.head_dim, n = tb.n_kv_heads * dh, qpk = tb.q_per_kv;
@@ -1430,7 +1437,8 @@ hipError_t launch_upproj(const dckv_plan& p, int32_t batch_rows, const float* am
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, dim3(p.dh / ctm, p.Hkv, (rows + 63) / 64), dim3(256), lds, stream,
+    const int ngr = p.Hkv * ((rows + 63) / 64);
+    hipLaunchKernelGGL(kern, dim3(8 * ((ngr + 7) / 8) * (p.dh / ctm)), dim3(256), lds, stream,
                        amerged, static_cast<const bf16*>(R_value), out, rows, p.rv, p.tables);
     return hipGetLastError();
   }

@@ -70,6 +70,12 @@ SMALL = {
     "valu_bf16": dict(hidden=2560, num_q_heads=32, num_kv_heads=32, head_dim=128,
                       sizes=(8, 8, 8, 8), group_rank=(300, 200, 100, 50), value_rank=2304,
                       seq_lens=(200, 70), permute_pages=False, split=128),
+    # more sequences than the query fold stages at once (64), short and
+    # empty ones among them, and more than 64 rows a KV head
+    "many_seqs": dict(hidden=512, num_q_heads=8, num_kv_heads=8, head_dim=64, sizes=(3, 5),
+                      group_rank=(96, 40), value_rank=128,
+                      seq_lens=tuple((37 * i) % 201 for i in range(70)), permute_pages=True,
+                      split=64),
     # groups of 8, 12 and 12 rows: the plan cuts the smallest group, so one
     # 16-row tile loads two separate ranges of key chunks
     "gqa_reordered": dict(hidden=512, num_q_heads=32, num_kv_heads=8, head_dim=64, sizes=(2, 3, 3),
