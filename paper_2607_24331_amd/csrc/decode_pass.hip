@@ -1110,22 +1110,25 @@ __global__ __launch_bounds__(1024) void upproj_wide(const float* __restrict__ am
 // ---------------------------------------------------------------------------
 // Up-projection on MFMA: o[row][c] = sum_r a[row][r] R_v[r][kv d_h + c] for
 // the rows of one KV head (sequence, query, head of the KV head).  One
-// work-group of four waves a (column tile of CT, KV head, group of 64
-// rows).  The work-group's R_v block (r_v x CT bf16) is loaded once, in 8 x 8 units
+// work-group of W waves (4, or 8 when a wave would otherwise walk 32 rank
+// steps or more) a (column tile of CT, KV head, group of 64 rows).  The work-group's R_v block (r_v x CT bf16) is loaded once, in 8 x 8 units
 // transposed in registers, and stored in LDS rank-contiguous per column:
 // the MFMA's B operand takes 8 consecutive ranks of one column a lane.  The
-// waves are the row group's 16-row tiles (1, 2 or 4) times KS = 4 / tiles
+// waves are the row group's 16-row tiles (1, 2 or 4) times KS = W / tiles
 // rank ranges; a wave's A operand is its 16 merged rows (fp32 split into
 // bf16 hi + lo parts) read from global memory in operand order, KA rank
 // steps ahead.  The rank ranges' sums are added through LDS in a fixed
 // order.
-template <int CT>
-__global__ __launch_bounds__(256) void upproj_mfma(const float* __restrict__ amerged,
+constexpr int kUpWavesMax = 8;                 // waves of the MFMA up-projection, at most
+
+template <int CT, int W>
+__global__ __launch_bounds__(W * 64) void upproj_mfma(const float* __restrict__ amerged,
                                                    const bf16* __restrict__ Rv,
                                                    float* __restrict__ out, int rows, int rv,
                                                    HeadTables tb) {
   constexpr int NC = CT / 16;                  // column tiles of a wave
-  constexpr int KA = 4;                        // rank steps of A loads in flight
+  constexpr int KA = W == 8 ? 8 : 4;           // rank steps of A loads in flight
+  constexpr int NTH = W * 64;
   constexpr int UB = 2;                        // R_v units (8 x 8) a thread a batch
   extern __shared__ __align__(16) unsigned char smem[];
   bf16* rt = reinterpret_cast<bf16*>(smem);    // [CT][stride]
@@ -1142,7 +1145,7 @@ __global__ __launch_bounds__(256) void upproj_mfma(const float* __restrict__ ame
   const int dh = tb.head_dim, n = tb.n_kv_heads * dh, qpk = tb.q_per_kv;
   const int nrow = min(64, rows - row0);
   const int tiles = nrow <= 16 ? 1 : (nrow <= 32 ? 2 : 4);
-  const int KS = 4 / tiles;
+  const int KS = W / tiles;
   const int mt = w % tiles, ks = w / tiles;
   const int nstep = (rv + 31) >> 5;            // 32-rank steps
   const int stride = 32 * nstep + 8;           // LDS row of one column (elements)
@@ -1175,11 +1178,11 @@ __global__ __launch_bounds__(256) void upproj_mfma(const float* __restrict__ ame
   // 16-byte row loads, transposed in registers into eight rank-contiguous
   // 16-byte column pieces; ranks past r_v are stored as zero
   const int nunit = 4 * nstep * (CT / 8);
-  for (int base = 0; base < nunit; base += 256 * UB) {
+  for (int base = 0; base < nunit; base += NTH * UB) {
     u32x4 v[UB][8];
 #pragma unroll
     for (int k = 0; k < UB; ++k) {
-      const int u = min(base + tid + 256 * k, nunit - 1);
+      const int u = min(base + tid + NTH * k, nunit - 1);
       const int r0 = 8 * (u / (CT / 8)), c8 = 8 * (u % (CT / 8));
 #pragma unroll
       for (int i = 0; i < 8; ++i)
@@ -1187,7 +1190,7 @@ __global__ __launch_bounds__(256) void upproj_mfma(const float* __restrict__ ame
     }
 #pragma unroll
     for (int k = 0; k < UB; ++k) {
-      const int u = base + tid + 256 * k;
+      const int u = base + tid + NTH * k;
       if (u < nunit) {
         const int r0 = 8 * (u / (CT / 8)), c8 = 8 * (u % (CT / 8));
 #pragma unroll
@@ -1396,7 +1399,7 @@ hipError_t launch_score(const dckv_plan& p, const DecodeShape& sh, const u32x4* 
 
 size_t upproj_mfma_lds_bytes(const dckv_plan& p, int ct) {
   const size_t stride = size_t((p.rv + 31) / 32) * 32 + 8;
-  return std::max<size_t>(size_t(ct) * stride * 2, size_t(4) * (ct / 16) * 64 * 16);
+  return std::max<size_t>(size_t(ct) * stride * 2, size_t(kUpWavesMax) * (ct / 16) * 64 * 16);
 }
 
 size_t upproj_wide_lds_bytes(const dckv_plan& p, int rows, int rb) {
@@ -1433,12 +1436,16 @@ hipError_t launch_upproj(const dckv_plan& p, int32_t batch_rows, const float* am
                   : (fit32 && (groups * (p.dh / 32) >= 256 || !fit16)) ? 32 : (fit16 ? 16 : 0);
   if (ctm) {
     const size_t lds = upproj_mfma_lds_bytes(p, ctm);
-    auto kern = ctm == 32 ? upproj_mfma<32> : upproj_mfma<16>;
+    // eight waves when four would each walk 32 rank steps or more
+    const int tiles = rows <= 16 ? 1 : (rows <= 32 ? 2 : 4);
+    const int W = ((p.rv + 31) / 32) * tiles / 4 >= 32 ? 8 : 4;
+    auto kern = ctm == 32 ? (W == 8 ? upproj_mfma<32, 8> : upproj_mfma<32, 4>)
+                          : (W == 8 ? upproj_mfma<16, 8> : upproj_mfma<16, 4>);
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
     if (e != hipSuccess) return e;
     const int ngr = p.Hkv * ((rows + 63) / 64);
-    hipLaunchKernelGGL(kern, dim3(8 * ((ngr + 7) / 8) * (p.dh / ctm)), dim3(256), lds, stream,
+    hipLaunchKernelGGL(kern, dim3(8 * ((ngr + 7) / 8) * (p.dh / ctm)), dim3(W * 64), lds, stream,
                        amerged, static_cast<const bf16*>(R_value), out, rows, p.rv, p.tables);
     return hipGetLastError();
   }

@@ -70,6 +70,15 @@ SMALL = {
     "valu_bf16": dict(hidden=2560, num_q_heads=32, num_kv_heads=32, head_dim=128,
                       sizes=(8, 8, 8, 8), group_rank=(300, 200, 100, 50), value_rank=2304,
                       seq_lens=(200, 70), permute_pages=False, split=128),
+    # 40 rows a KV head and value rank 1024: the eight-wave up-projection
+    "rows40_rv1024": dict(hidden=1024, num_q_heads=8, num_kv_heads=8, head_dim=128, sizes=(3, 5),
+                          group_rank=(64, 100), value_rank=1024,
+                          seq_lens=tuple((13 * i + 1) % 90 for i in range(40)),
+                          permute_pages=False, split=64),
+    # head size 96: the per-sequence query fold and the narrow up-projections
+    "head96": dict(hidden=384, num_q_heads=8, num_kv_heads=4, head_dim=96, sizes=(1, 3),
+                   group_rank=(50, 130), value_rank=144, seq_lens=(250, 3, 70),
+                   permute_pages=True, split=64),
     # more sequences than the query fold stages at once (64), short and
     # empty ones among them, and more than 64 rows a KV head
     "many_seqs": dict(hidden=512, num_q_heads=8, num_kv_heads=8, head_dim=64, sizes=(3, 5),
