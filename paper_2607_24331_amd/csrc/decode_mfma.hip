@@ -164,7 +164,14 @@ __global__ __launch_bounds__(64) void fold_mfma(const float* __restrict__ q,
                                                 u32x4* __restrict__ qblk_ws, int batch, float scale,
                                                 HeadTables tb, MfmaTables mt) {
   const int J = mt.n_slices;
-  const int slice = blockIdx.x / 16, j = blockIdx.x % 16, pr = blockIdx.y;
+  // 1-D grid, XCD-aware: the 16 slots of one (slice, chunk) write
+  // interleaved 16-byte pieces of the same blocks, so they share an XCD
+  // (work-group ids equal mod 8) and its L2 merges the pieces
+  const int ngrp = J * mt.max_pairs;
+  const int xcd = blockIdx.x & 7, pos = blockIdx.x >> 3;
+  const int grp = 8 * (pos >> 4) + xcd, j = pos & 15;
+  if (grp >= ngrp) return;
+  const int slice = grp / mt.max_pairs, pr = grp % mt.max_pairs;
   const int nch0 = mt.kln[slice][0][0] + mt.kln[slice][0][1];
   const int npairs = nch0 + (mt.nt > 1 ? mt.kln[slice][1][0] + mt.kln[slice][1][1] : 0);
   if (pr >= npairs) return;
@@ -999,7 +1006,8 @@ hipError_t launch_fold(const dckv_plan& p, const MfmaTables& mt, int32_t batch, 
   // MFMA; other head sizes: one wave a (sequence, slice, slot, chunk)
   if (p.dh == 64 || p.dh == 128) {
     auto kern = p.dh == 64 ? fold_mfma<2> : fold_mfma<4>;
-    hipLaunchKernelGGL(kern, dim3(mt.n_slices * 16, mt.max_pairs), dim3(64), 0, stream, q,
+    const int ngrp = mt.n_slices * mt.max_pairs;
+    hipLaunchKernelGGL(kern, dim3(8 * 16 * ((ngrp + 7) / 8)), dim3(64), 0, stream, q,
                        static_cast<const bf16*>(R_keys), static_cast<u32x4*>(qblk), batch, scale,
                        p.tables, mt);
     return hipGetLastError();
