@@ -20,7 +20,7 @@
 //
 // merge_mfma: fixed ascending-split log-sum-exp merge of the partials into
 // the normalised value-latent output a_h (fp32).
-// The up-projection o_h = a_h R_v[:, kv(h) block] is upproj_rows (decode_pass.hip).
+// The up-projection o_h = a_h R_v[:, kv(h) block] is launch_upproj (decode_pass.hip).
 #include <cmath>
 
 #include "device.h"

@@ -21,7 +21,8 @@
 //   order.  Partials: (E, L) and acc of the chunk's rank group.
 // merge_chunks: the chunks of each (sequence, head) merged in ascending order
 //   into the normalised value-latent row a_h.
-// upproj_rows: o_h = a_h R_v[:, kv(h) block] (Sec. III-A z R, Sec. III-D R_v).
+// upproj_wide / upproj_rows / upproj_mfma: o_h = a_h R_v[:, kv(h) block]
+//   (Sec. III-A z R, Sec. III-D R_v), by the number of rows a KV head.
 #include <algorithm>
 #include <cmath>
 
@@ -1409,14 +1410,15 @@ size_t upproj_wide_lds_bytes(const dckv_plan& p, int rows, int rb) {
 hipError_t launch_upproj(const dckv_plan& p, int32_t batch_rows, const float* amerged,
                          const void* R_value, float* out, hipStream_t stream) {
   const int rows = batch_rows * p.qpk;          // rows a KV head
-  // at most 4 rows a KV head, with 64-column tiles that give the grid at
+  // one or two rows a KV head, with 64-column tiles that give the grid at
   // least 32 work-groups: the wide kernel (whole 128-byte pieces of R_v;
-  // more rows would not fit its registers)
-  if (rows > 0 && rows <= 4 && p.dh % 64 == 0 && p.Hkv * (p.dh / 64) >= 32) {
-    const int rb = rows <= 1 ? 1 : (rows <= 2 ? 2 : 4);
+  // from three rows on its per-lane products cost more than the MFMA
+  // kernel's R_v transpose)
+  if (rows > 0 && rows <= 2 && p.dh % 64 == 0 && p.Hkv * (p.dh / 64) >= 32) {
+    const int rb = rows <= 1 ? 1 : 2;
     const size_t lds = upproj_wide_lds_bytes(p, rows, rb);
     if (lds <= 160 * 1024) {
-      auto kern = rb == 1 ? upproj_wide<1> : (rb == 2 ? upproj_wide<2> : upproj_wide<4>);
+      auto kern = rb == 1 ? upproj_wide<1> : upproj_wide<2>;
       hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                          hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
       if (e != hipSuccess) return e;
@@ -1425,14 +1427,14 @@ hipError_t launch_upproj(const dckv_plan& p, int32_t batch_rows, const float* am
       return hipGetLastError();
     }
   }
-  // MFMA for at least 8 rows a KV head (fewer: R_v is read once either way
-  // and the VALU kernel reads it straight into registers): 32-column tiles
+  // MFMA for at least 3 rows a KV head (fewer: R_v is read once either way
+  // and the VALU kernels read it straight into registers): 32-column tiles
   // while the transposed R_v block fits LDS and the grid still fills the
   // chip, else 16
   const int groups = p.Hkv * ((rows + 63) / 64);
   const bool fit32 = p.dh % 32 == 0 && upproj_mfma_lds_bytes(p, 32) <= 160 * 1024;
   const bool fit16 = p.dh % 16 == 0 && upproj_mfma_lds_bytes(p, 16) <= 160 * 1024;
-  const int ctm = rows < 8 ? 0
+  const int ctm = rows < 3 ? 0
                   : (fit32 && (groups * (p.dh / 32) >= 256 || !fit16)) ? 32 : (fit16 ? 16 : 0);
   if (ctm) {
     const size_t lds = upproj_mfma_lds_bytes(p, ctm);
