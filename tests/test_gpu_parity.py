@@ -200,7 +200,8 @@ def test_launch_shapes_cover_both_rings():
 # 32 heads x 8 queries fill all eight row slices of the MFMA path; f32 runs
 # the portable kernels.
 MULTI = [("gqa_uneven", 4, "bf16"), ("mha32_two_tiles", 2, "bf16"), ("mha32_two_tiles", 8, "bf16"),
-         ("mha_odd", 8, "bf16"), ("singletons", 3, "bf16"), ("mha_odd", 3, "f32")]
+         ("mha_odd", 8, "bf16"), ("singletons", 3, "bf16"), ("mha_odd", 3, "f32"),
+         ("many_seqs", 2, "bf16")]
 
 
 @pytest.mark.parametrize("name, Q, dtype", MULTI)
@@ -476,6 +477,43 @@ def test_value_rank_3072_full_layer_both_kernel_sets():
         outs.append(out)
         del pool
     assert np.max(np.abs(outs[0] - outs[1])) <= 1e-2 * np.max(np.abs(outs[0]))
+
+
+@pytest.mark.parametrize("n", [1, 129, 640])
+def test_append_mfma_ragged_token_counts_reproducible(n):
+    # one token, one past a 128-token tile, and five full tiles through the
+    # MFMA kernel (hidden 512: eight 64-deep stages, four stage buffers): each
+    # latent within one bf16 ulp of the rounded exact product, and a second
+    # call writes the same bits
+    hidden = 512
+    wl = custom_workload(name="append_n", seed=78, hidden=hidden, num_q_heads=4, num_kv_heads=4,
+                         head_dim=64, group_of_kv=(0, 1, 1, 0), group_rank=(50, 61), value_rank=100,
+                         dtype="bf16", batch=1, seq_lens=(n,), prefill_lens=(n,))
+    g = np.random.default_rng(n)
+    from workloads.inputs import to_storage
+    x = to_storage(g.standard_normal((n, hidden)), "bf16")
+    Lk = to_storage(g.standard_normal((hidden, 111)) / np.sqrt(hidden), "bf16")
+    Lv = to_storage(g.standard_normal((hidden, 100)) / np.sqrt(hidden), "bf16")
+    npages = (n + 63) // 64
+    table = np.arange(npages, dtype=np.int32)[None, :]
+    slots = np.arange(n, dtype=np.int64)
+    plan = plan_for(wl)
+    from paper_2607_24331_amd import latent_append
+    pools = []
+    for _ in range(2):
+        pool = plan.new_pool(npages)
+        latent_append(plan, dev(x, "bf16"), dev(Lk.T, "bf16"), dev(Lv.T, "bf16"),
+                      torch.from_numpy(slots).cuda(), pool)
+        torch.cuda.synchronize()
+        pools.append(pool.view(torch.int16).cpu().numpy().copy())
+        last = pool
+    assert np.array_equal(pools[0], pools[1])
+    Zk_g, Zv_g = olayout.unpack(last.float().cpu().numpy(), table, 0, n, 111, 100)
+    for Zg, L in ((Zk_g, Lk), (Zv_g, Lv)):
+        exact = oappend.down_project(x, L)
+        rounded = obf16.round_to_bf16(exact)
+        bound = obf16.ulp_bf16(rounded) + hidden * 2.0 ** -24 * oappend.abs_bound(x, L)
+        assert np.all(np.abs(Zg - rounded) <= bound)
 
 
 @pytest.mark.parametrize("hidden", [200, 320, 384, 512])
