@@ -125,7 +125,7 @@ __device__ __forceinline__ u32x4 scale8(u32x4 v, float f) {
 //          for every block and page of the unit; -inf for a row with no
 //          visible token in the unit), l the sum of the block's weights as
 //          stored
-template <int NT, int RING>
+template <int NT, int RING, bool MASK>
 __global__ __launch_bounds__(512, 1) void score_pages(
     const u32x4* __restrict__ qblk_ws, const bf16* __restrict__ pool, int64_t num_pages,
     const int32_t* __restrict__ page_table, int max_pages, const int32_t* __restrict__ seq_lens,
@@ -277,7 +277,10 @@ __global__ __launch_bounds__(512, 1) void score_pages(
 
   auto consume = [&](u32x4 a) {
     const int c = con_c < ln0 ? st0 + con_c : st1 + (con_c - ln0);
-    if (c == kc_last) a = keep_first(a, kvalid_last);
+    // MASK: R_K is not a multiple of 32, so the last key chunk holds padding
+    // columns (zero when written by the append, but masked all the same);
+    // without it the check and its selects are compiled out
+    if (MASK && c == kc_last) a = keep_first(a, kvalid_last);
     S = mfma(a, bhi, S);
     S = mfma(a, blo, S);
     // the next item's query blocks
@@ -1373,7 +1376,7 @@ hipError_t launch_score_r(const dckv_plan& p, const DecodeShape& sh, const u32x4
                           const void* pool, int64_t num_pages, const int32_t* page_table,
                           int32_t max_pages, const int32_t* seq_lens, uint32_t* pw,
                           hipStream_t stream) {
-  auto kern = score_pages<NT, RING>;
+  auto kern = p.RK % 32 ? score_pages<NT, RING, true> : score_pages<NT, RING, false>;
   const size_t lds = pass_score_lds_bytes(p);
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
@@ -1393,7 +1396,6 @@ hipError_t launch_score(const dckv_plan& p, const DecodeShape& sh, const u32x4* 
                         hipStream_t stream) {
   switch (p.pass_ring) {
     case 16: return launch_score_r<NT, 16>(p, sh, qblk, pool, num_pages, page_table, max_pages, seq_lens, pw, stream);
-    case 32: return launch_score_r<NT, 32>(p, sh, qblk, pool, num_pages, page_table, max_pages, seq_lens, pw, stream);
   }
   return hipErrorInvalidValue;
 }

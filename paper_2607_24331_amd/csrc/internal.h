@@ -130,7 +130,7 @@ struct dckv_plan {
   dckv::MfmaTables mfma{};
   bool pass_ok = false;              // bf16 two-pass decode applies (<= 256 (query, head) rows)
   dckv::MfmaTables pass{};           // its tables: slices of <= 32 rows, fewest chunk loads
-  int32_t pass_ring = 0;             // score-pass loads in flight a wave (16 or 32)
+  int32_t pass_ring = 0;             // score-pass loads in flight a wave (16; 32 measured slower)
   int32_t key_chunk_loads = 0;       // key chunks the MFMA tiles load a page
   dckv::RopeTables rope{};           // rotary decode tables (valid with mfma_ok)
   int64_t rope_rt_elems = 0;         // elements of the transposed key factors
