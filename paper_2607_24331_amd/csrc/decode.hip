@@ -326,7 +326,8 @@ DecodeShape decode_shape(const dckv_plan& p, int32_t batch, int32_t max_context)
   if (s.mfma) {
     const int64_t units = int64_t(batch) * s.n_split;
     s.n_units = int32_t((units + 7) / 8 * 8);
-    s.n_rchunks = mfma_merge_rank_chunks(p);
+    s.merge_ranks = mfma_merge_ranks(p, batch);
+    s.n_rchunks = (p.rv + s.merge_ranks - 1) / s.merge_ranks;
     const size_t nh = 16 * size_t(p.mfma.nt);
     const size_t rows = size_t(batch) * p.mfma.n_slices * s.n_split;
     s.off_acc = s.off_ml + align_up(rows * 2 * nh * sizeof(float), 256);

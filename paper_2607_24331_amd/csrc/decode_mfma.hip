@@ -35,7 +35,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kPageSlots = 256;           // pages per split the LDS page list holds
 constexpr int kPStride = 72;              // bf16 per head row of the p tile (64 + pad)
-constexpr int kMergeRanks = 8;            // value ranks per merge work-group
+constexpr int kMergeRanks = 8;            // value ranks per merge work-group (16 for deep batches)
 constexpr int kQblkLoads = 16;            // folded-query loads a thread issued at the split's start
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -711,24 +711,26 @@ __global__ __launch_bounds__(W * 64, 1) void split_mfma(
 
 // ---------------------------------------------------------------------------
 // Merge: a[b][h][r] = sum_s 2^(m_s - M) acc_s[r] / sum_s 2^(m_s - M) l_s.
-// Grid (batch * slices, value-rank chunks of kMergeRanks), 256 threads.
+// Grid (batch * slices, value-rank chunks of MR), 256 threads; MR = 8, or 16
+// when the grid would hold 2048 work-groups or more (deep batches: fewer,
+// larger work-groups, each reading the (m, l) rows once for more ranks).
 // Pass 1: per head slot the maximum M and the weighted sum L over splits,
 // read from the compact (m, l) rows, up to 32 (16 pairs) independent loads
 // a thread for long merges, eight for short ones.
-// Pass 2: a split row of the chunk is kMergeRanks * NH contiguous floats;
+// Pass 2: a split row of the chunk is MR * NH contiguous floats;
 // TPR threads cover it with float4 loads (4 head slots each) and the
 // 256 / TPR thread groups take the splits round-robin, sixteen splits in
 // flight for long merges, four for short ones.
 // Fixed order: group g sums splits g, g + G, ... ascending, then the G group
 // sums are added in order.
-template <int NH, bool LONG>
+template <int NH, bool LONG, int MR>
 __global__ __launch_bounds__(256) void merge_mfma(const float* __restrict__ part_ml,
                                                   const float* __restrict__ part,
                                                   const int32_t* __restrict__ seq_lens,
                                                   int max_context, int split_tokens, int n_split,
                                                   int rv, float* __restrict__ amerged,
                                                   HeadTables tb, MfmaTables mt) {
-  constexpr int TPR = kMergeRanks * NH / 4;   // threads a split row
+  constexpr int TPR = MR * NH / 4;            // threads a split row
   constexpr int G = 256 / TPR;                // split groups
   constexpr int SUB = 256 / NH;               // split groups of pass 1
   const int bj = blockIdx.x;                  // (sequence, slice) on x: grid x is wide
@@ -813,7 +815,7 @@ __global__ __launch_bounds__(256) void merge_mfma(const float* __restrict__ part
   const int g = tid / TPR, e = tid % TPR;
   const int rl = e / (NH / 4);                 // rank inside the chunk
   const int hq = (e % (NH / 4)) * 4;           // first of four head slots
-  const int r = rc * kMergeRanks + rl;
+  const int r = rc * MR + rl;
   const float4 M4 = make_float4(sM[hq], sM[hq + 1], sM[hq + 2], sM[hq + 3]);
   float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
   if (r < rv) {
@@ -987,8 +989,11 @@ hipError_t launch_merge_upproj(const dckv_plan& p, const DecodeShape& sh, const 
   // the deep-batch merge only for long split lists: its registers would cost
   // the short merges (many small work-groups) their occupancy
   const bool lng = sh.n_split >= 128;
-  auto kern = p.mfma.nt == 1 ? (lng ? merge_mfma<16, true> : merge_mfma<16, false>)
-                             : (lng ? merge_mfma<32, true> : merge_mfma<32, false>);
+  auto kern = sh.merge_ranks == 16
+                  ? (p.mfma.nt == 1 ? (lng ? merge_mfma<16, true, 16> : merge_mfma<16, false, 16>)
+                                    : (lng ? merge_mfma<32, true, 16> : merge_mfma<32, false, 16>))
+                  : (p.mfma.nt == 1 ? (lng ? merge_mfma<16, true, 8> : merge_mfma<16, false, 8>)
+                                    : (lng ? merge_mfma<32, true, 8> : merge_mfma<32, false, 8>));
   hipLaunchKernelGGL(kern, dim3(sh.batch * p.mfma.n_slices, sh.n_rchunks), dim3(256), 0, stream,
                      part_ml, part, seq_lens, sh.max_context, sh.split_tokens, sh.n_split, p.rv,
                      amerged, p.tables, p.mfma);
@@ -1022,7 +1027,10 @@ size_t mfma_split_lds_bytes(const dckv_plan& p) {
   return size_t(p.mfma.max_pairs) * 2048 + 32 * kPStride * 2 + 2 * 8 * 32 * 4 + kPageSlots * 4;
 }
 
-int mfma_merge_rank_chunks(const dckv_plan& p) { return (p.rv + kMergeRanks - 1) / kMergeRanks; }
+int mfma_merge_ranks(const dckv_plan& p, int32_t batch) {
+  const int64_t groups = int64_t(batch) * p.mfma.n_slices * ((p.rv + kMergeRanks - 1) / kMergeRanks);
+  return groups >= 2048 ? 2 * kMergeRanks : kMergeRanks;
+}
 
 int mfma_max_split_tokens() { return kPageSlots * DCKV_PAGE_TOKENS; }
 

@@ -87,6 +87,7 @@ struct DecodeShape {
   bool pass;                // bf16 two-pass MFMA path (score_pages, value_pages)
   int32_t n_units;          // batch * n_split rounded up to a multiple of 8: grid units (MFMA path)
   int32_t n_rchunks;        // value-rank chunks of the merge (MFMA path)
+  int32_t merge_ranks = 8;  // value ranks a merge work-group (8 or 16)
   // two-pass path
   int32_t npm;              // pages of the longest sequence: ceil(max_context / 64), at least 1
   int32_t unit_pages;       // pages a score work-group
@@ -180,7 +181,7 @@ hipError_t launch_fold(const dckv_plan& p, const MfmaTables& mt, int32_t batch, 
 
 // MFMA decode path (decode_mfma.hip).
 size_t mfma_split_lds_bytes(const dckv_plan& p);
-int mfma_merge_rank_chunks(const dckv_plan& p);
+int mfma_merge_ranks(const dckv_plan& p, int32_t batch);   // value ranks a merge work-group
 int mfma_max_split_tokens();
 hipError_t launch_decode_mfma(const dckv_plan& p, const DecodeShape& sh, const float* q,
                               const void* pool, int64_t num_pages, const int32_t* page_table,
