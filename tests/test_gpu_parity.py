@@ -389,6 +389,28 @@ def test_full_workload_sampled_rows(name):
     assert max(errs) <= TOL_REL_ROW
 
 
+def test_long_split_list_deep_batch_merge():
+    # 128 splits of 64 tokens over 16 sequences and value rank 1024: the
+    # merge for long split lists with sixteen value ranks a work-group
+    wl = custom_workload(name="deep_long", seed=91, hidden=1024, num_q_heads=8, num_kv_heads=8,
+                         head_dim=128, group_of_kv=(0, 0, 0, 1, 1, 1, 1, 1),
+                         group_rank=(96, 160), value_rank=1024, dtype="bf16", batch=16,
+                         seq_lens=tuple(8192 - 517 * (i % 5) for i in range(16)),
+                         factor_scheme="orthonormal")
+    inp = make_inputs(wl)
+    plan = plan_for(wl, 64)
+    info = plan.launch_info(wl.batch, max(wl.seq_lens))
+    assert info["split_tokens"] == 64
+    pool = gpu_pool_with_append(inp, plan)
+    out = run_decode(inp, plan, pool)
+    assert np.array_equal(out, run_decode(inp, plan, pool))
+    pairs = sample_pairs(wl, 8)
+    ref = oracle_rows(inp, pairs)
+    errs = [row_rel_err(out[b, h], ref[(b, h)]) for b, h in pairs]
+    _report("deep_long", errs)
+    assert max(errs) <= TOL_REL_ROW
+
+
 def every_sequence_pairs(wl):
     """One (sequence, head) row of every sequence; sequence b takes a head of
     group b mod G (the group's heads in turn), so every group is covered."""
