@@ -411,6 +411,25 @@ def test_long_split_list_deep_batch_merge():
     assert max(errs) <= TOL_REL_ROW
 
 
+def test_wide_up_projection_tiles_many_rows():
+    # 70 rows over 32 KV heads of 128 (two 64-row groups a head): the grid
+    # holds 256 (KV head, row group, 32-column tile) work-groups, so the MFMA
+    # up-projection takes 32-column tiles; every row checked
+    wl = custom_workload(name="mha32_b70", seed=92, hidden=4096, num_q_heads=32, num_kv_heads=32,
+                         head_dim=128, group_of_kv=tuple(i // 8 for i in range(32)),
+                         group_rank=(64, 96, 40, 72), value_rank=256, dtype="bf16", batch=70,
+                         seq_lens=tuple(1 + (29 * i) % 150 for i in range(70)),
+                         factor_scheme="orthonormal")
+    inp = make_inputs(wl)
+    plan = plan_for(wl)
+    pool = gpu_pool_with_append(inp, plan)
+    out = run_decode(inp, plan, pool)
+    ref = _all_rows(inp)
+    errs = [row_rel_err(out[b, h], o) for (b, h), o in ref.items()]
+    _report("mha32_b70", errs)
+    assert max(errs) <= TOL_REL_ROW
+
+
 def every_sequence_pairs(wl):
     """One (sequence, head) row of every sequence; sequence b takes a head of
     group b mod G (the group's heads in turn), so every group is covered."""
